@@ -1,0 +1,13 @@
+"""CPU oracle for the refinement step -- test infrastructure only.
+
+Plain float64 NumPy (plus a small C weight generator) implementation of one
+refinement step and of the refine loop, written from the paper's description
+(Sec. 4.2, App. C.4).  Only tests/, the smoke check and the benchmark's
+CPU-baseline leg may import it.  It shares no code with the GPU library.
+"""
+
+from .weights import OracleWeights, philox4x32_10, tensor_id  # noqa: F401
+from .refine import (  # noqa: F401
+    attention, edit_rule, forward, layer_forward, lm_head_reduce, moe_ffn, refine, refine_step,
+    rms_norm, rope, route, softmax, swiglu,
+)
