@@ -1,0 +1,198 @@
+/*
+ * dlm.h -- C ABI of the MI355X (gfx950) refinement-step library.
+ *
+ * The library runs the refinement stage of draft-then-refine decoding for
+ * diffusion language models (paper: Sec. 4.2 "Bidirectional Refinement"):
+ * the refiner receives a fixed prompt and a complete draft, runs a
+ * bidirectional (non-causal) transformer forward over the whole sequence,
+ * reduces each draft position's vocabulary logits to a top-1 token and its
+ * confidence, and applies a threshold rule that re-edits draft tokens and
+ * unmasks [MASK] positions.  The pass budget is an upper bound: the loop stops
+ * once a pass changes nothing (App. C.4; one refine threshold, Table 10).
+ *
+ * Conventions for every entry point
+ *   - Pointers named d_* are device pointers (HIP device memory on the current
+ *     device); h_* are host pointers.  The caller owns every buffer: weights,
+ *     workspace, tokens and outputs.  The library owns only the small host
+ *     handle returned by dlm_load_synthetic_weights, freed by dlm_free.
+ *   - hip_stream is a hipStream_t passed as void* (NULL = the default stream).
+ *     All device work is enqueued on it; entry points return without waiting
+ *     unless stated.
+ *   - Return value: DLM_OK (0) or a negative dlm_status.  On error nothing is
+ *     launched, and dlm_last_error() returns a message (thread-local).  No C++
+ *     exception crosses this boundary.
+ *   - Integers are int32 unless stated; token arrays are row-major int32
+ *     [batch][len].  Floats are IEEE binary32.
+ */
+#ifndef DLM_H
+#define DLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DLM_OK = 0,
+    DLM_ERR_INVALID_ARG = -1,   /* bad shape, null pointer, non-finite threshold ... */
+    DLM_ERR_HIP = -3,           /* a HIP runtime call failed                          */
+    DLM_ERR_UNSUPPORTED = -4,   /* a shape the kernels do not implement              */
+    DLM_ERR_WORKSPACE = -5      /* weights or workspace buffer too small             */
+} dlm_status;
+
+/*
+ * Refiner shape.  Architecture (the paper does not describe the refiner's
+ * internals, Sec. 5.1): pre-norm RMSNorm blocks, rotate-half RoPE on q and k
+ * with positions 0..S-1 of each sequence, non-causal grouped-query attention,
+ * then either a dense SwiGLU FFN (n_experts == 0) or a softmax-routed top-k
+ * SwiGLU mixture of experts renormalised over the k selected, plus
+ * n_shared_experts (0 or 1) always-on experts of width expert_ffn_dim; a final
+ * RMSNorm and an untied LM head.  mask_id is the [MASK] token id.
+ * Supported: head_dim 64 or 128; d_model, n_heads*head_dim multiples of 128;
+ * ffn widths multiples of 64; n_experts <= 256; top_k <= 8; vocab >= 2.
+ */
+typedef struct dlm_config {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t n_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t ffn_dim;           /* dense SwiGLU width (n_experts == 0)           */
+    int32_t n_experts;         /* routed experts, 0 = dense FFN                  */
+    int32_t top_k;
+    int32_t expert_ffn_dim;    /* width of routed and shared experts            */
+    int32_t n_shared_experts;  /* 0 or 1                                        */
+    int32_t vocab;
+    int32_t mask_id;           /* 0 <= mask_id < vocab                          */
+    float rope_theta;          /* e.g. 10000                                    */
+    float norm_eps;            /* e.g. 1e-6                                     */
+    float init_std;            /* synthetic weight standard deviation (0.02)    */
+    float lm_head_scale;       /* extra factor on the LM head's init std (1.0)  */
+} dlm_config;
+
+typedef struct dlm_model dlm_model;   /* opaque host handle */
+
+/* Counters of one pass or of a whole refine call. */
+typedef struct dlm_stats {
+    int32_t n_unmasked;     /* [MASK] slots that took a token                    */
+    int32_t n_edited;       /* real-token slots that changed                     */
+    int32_t n_masked_left;  /* [MASK] slots left at the end (dlm_refine only)    */
+    int32_t steps_run;      /* passes executed (dlm_refine only)                 */
+} dlm_stats;
+
+/* Bytes of device memory the weights of cfg occupy (0 if cfg is invalid). */
+size_t dlm_weights_bytes(const dlm_config* cfg);
+
+/* Bytes of device workspace one pass over a [batch][prompt_len + draft_len]
+ * token array needs (0 if the arguments are invalid). */
+size_t dlm_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len,
+                           int32_t draft_len);
+
+/*
+ * Fill d_weights (>= dlm_weights_bytes(cfg) bytes, 256-byte aligned) with the
+ * synthetic weights of cfg for `seed`, on hip_stream, and return a handle in
+ * *out.  Weight element i (row-major in the logical [out_features x
+ * in_features] matrix) of tensor `tid` is
+ *     n = sum of the four 16-bit halves of words 0,1 of
+ *         Philox4x32-10(counter = (i_lo, i_hi, tid, 0), key = (seed_lo, seed_hi))
+ *         minus 131070,
+ *     w = bf16_round_nearest_even(float(n) * float(init_std * s * sqrt(3) / 65536))
+ * with s = lm_head_scale for the LM head and 1 otherwise; tid =
+ * (layer_field << 20) | (kind << 12) | expert with layer_field 0 for the
+ * embedding (kind 0) and the LM head (kind 1), and l+1 for layer l with kinds
+ * Wq 0, Wk 1, Wv 2, Wo 3, dense gate 4 / up 5 / down 6, router 7, expert gate 8
+ * / up 9 / down 10, shared gate 11 / up 12 / down 13.  RMSNorm gains are 1.
+ * The handle keeps d_weights (not owned); the buffer must outlive it.
+ */
+dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void* d_weights,
+                                      size_t weights_bytes, void* hip_stream, dlm_model** out);
+
+/*
+ * One refinement pass (Sec. 4.2) over d_tokens [batch][prompt_len + draft_len]
+ * (in/out): forward over all positions with no attention mask, then for every
+ * draft position p the top-1 token t* (lowest id among equal maxima) and its
+ * confidence conf = 1 / sum_v exp(z_v - max z), then all draft positions are
+ * updated at once: a slot takes t* when t* != mask_id and conf >= threshold.
+ * Prompt slots are never written.  Draft slots may hold mask_id; the prompt
+ * may not (DLM_ERR_INVALID_ARG is not detectable on device: such a prompt is
+ * processed as an ordinary token).
+ * Optional outputs (NULL to skip), device pointers:
+ *   d_top1 int32 [batch][draft_len], d_conf float [batch][draft_len],
+ *   d_stats dlm_stats (n_unmasked, n_edited of this pass; other fields 0).
+ * threshold must not be NaN (any other float is accepted; > 1 edits nothing,
+ * <= 0 takes every top-1 that is not mask_id).
+ */
+dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                           int32_t* d_tokens, float threshold, void* d_workspace,
+                           size_t workspace_bytes, void* hip_stream, int32_t* d_top1,
+                           float* d_conf, dlm_stats* d_stats);
+
+/*
+ * Refine a draft: slots with d_mask[b][i] != 0 start as mask_id (d_mask may be
+ * NULL = empty mask set), then up to n_steps passes of dlm_refine_step,
+ * stopping after a pass that changed no slot.  d_prompt int32 [batch][prompt_len]
+ * is read only; d_draft int32 [batch][draft_len] is updated in place.  Blocks
+ * the calling thread once per pass (a 16-byte device-to-host copy) to decide the
+ * early stop.  h_stats (host, may be NULL) receives totals over all passes.
+ * n_steps = 0 only applies the mask set.
+ */
+dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                      const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask,
+                      int32_t n_steps, float threshold, void* d_workspace, size_t workspace_bytes,
+                      void* hip_stream, dlm_stats* h_stats);
+
+/*
+ * Test hooks (same kernels as dlm_refine_step, intermediate results exposed).
+ *
+ * dlm_debug_forward: forward over d_tokens without the reduction; writes the
+ *   residual stream after the last layer (before the final norm) to d_hidden
+ *   float [batch*(prompt_len+draft_len)][d_model], and, when d_max_logit is
+ *   not NULL, the per-draft-position max logit, top-1 and confidence of the
+ *   fused reduction to d_max_logit / d_top1 / d_conf [batch*draft_len].
+ *   When d_logits is not NULL it also writes full float logits of the draft
+ *   rows [batch*draft_len][vocab] through the same LM-head GEMM (test-only:
+ *   the refine path never materialises logits).
+ * dlm_debug_layer: one block `layer` applied to the float residual stream
+ *   d_x_in [batch*seq][d_model], result to d_x_out (may equal d_x_in).
+ * dlm_debug_head: final norm + LM head + fused reduction on a float residual
+ *   stream d_x [batch*(prompt_len+draft_len)][d_model] (draft rows used).
+ */
+dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                             const int32_t* d_tokens, void* d_workspace, size_t workspace_bytes,
+                             void* hip_stream, float* d_hidden, float* d_max_logit,
+                             int32_t* d_top1, float* d_conf, float* d_logits);
+dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len,
+                           const float* d_x_in, float* d_x_out, void* d_workspace,
+                           size_t workspace_bytes, void* hip_stream);
+dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                          const float* d_x, void* d_workspace, size_t workspace_bytes,
+                          void* hip_stream, float* d_max_logit, int32_t* d_top1, float* d_conf);
+
+/* Device pointer and byte size of one logical weight tensor (for tests):
+ * kind/layer/expert as in dlm_load_synthetic_weights; *d_ptr receives the
+ * base of the tensor's storage and *layout a code: 0 = plain row-major
+ * [out][in]; 1 = gate/up interleaved in 32-row blocks with its partner. */
+dlm_status dlm_weight_info(dlm_model* m, int32_t layer_field, int32_t kind, int32_t expert,
+                           void** d_ptr, int32_t* layout);
+
+/*
+ * Kernel timing with HIP events recorded on the launch stream around every
+ * launch whose kernel name equals name_filter ("*" = every launch, NULL = off).
+ * Recording restarts at each dlm_refine_step / dlm_refine call.
+ * dlm_profile_read waits for the recorded events and writes up to max_entries
+ * (kernel name, milliseconds) pairs, one per launch in launch order; it
+ * returns the number written, or -1 on error.  Names are static strings.
+ */
+dlm_status dlm_set_profiling(dlm_model* m, const char* name_filter);
+int32_t dlm_profile_read(dlm_model* m, const char** names, float* ms, int32_t max_entries);
+
+void dlm_free(dlm_model* m);
+const char* dlm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DLM_H */

@@ -1,0 +1,70 @@
+// Device-side helpers shared by the refinement-step kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;                                              // raw bfloat16 bits
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define DLM_WAVE 64
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+    return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// Round-to-nearest-even float -> bfloat16 (finite inputs; NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (bf16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Wave-wide reductions (64 lanes).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// Online-softmax partial over a set of logits: running max m, the lowest index
+// attaining it, and s = sum exp(z - m).  merge() is associative up to float
+// rounding and keeps the lower index on equal maxima.
+struct SoftmaxPartial {
+    float m;
+    int32_t idx;
+    float s;
+};
+
+__device__ __forceinline__ SoftmaxPartial sp_merge(SoftmaxPartial a, SoftmaxPartial b) {
+    SoftmaxPartial r;
+    if (b.m > a.m || (b.m == a.m && b.idx < a.idx)) {
+        r.m = b.m;
+        r.idx = b.idx;
+    } else {
+        r.m = a.m;
+        r.idx = a.idx;
+    }
+    float sa = (a.s == 0.f) ? 0.f : a.s * __expf(a.m - r.m);
+    float sb = (b.s == 0.f) ? 0.f : b.s * __expf(b.m - r.m);
+    r.s = sa + sb;
+    return r;
+}

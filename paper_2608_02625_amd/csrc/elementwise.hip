@@ -1,0 +1,233 @@
+// Bandwidth-bound kernels of the refinement pass: embedding gather, RMSNorm,
+// merge of the LM-head softmax partials, and the threshold edit/unmask rule.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// x[t][:] = E[tok[t]][:] (bf16 -> fp32); one workgroup per token.
+// Ids outside [0, V) are clamped into range so that no read leaves the table.
+__global__ void embed_kernel(const int32_t* __restrict__ tok, const bf16_t* __restrict__ emb,
+                             float* __restrict__ x, int d, int V) {
+    const int t = blockIdx.x;
+    const int id = min(max(tok[t], 0), V - 1);
+    const bf16_t* src = emb + (int64_t)id * d;
+    float* dst = x + (int64_t)t * d;
+    for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(src + i);
+        f32x4 lo, hi;
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+            lo[2 * w] = __uint_as_float(v[w] << 16);
+            lo[2 * w + 1] = __uint_as_float(v[w] & 0xffff0000u);
+            hi[2 * w] = __uint_as_float(v[w + 2] << 16);
+            hi[2 * w + 1] = __uint_as_float(v[w + 2] & 0xffff0000u);
+        }
+        *reinterpret_cast<f32x4*>(dst + i) = lo;
+        *reinterpret_cast<f32x4*>(dst + i + 4) = hi;
+    }
+}
+
+// h = bf16(x / sqrt(mean(x^2) + eps) * g), fp32 math; one workgroup (256) per row.
+__device__ __forceinline__ void rmsnorm_row(const float* __restrict__ xr, const bf16_t* __restrict__ g,
+                                            bf16_t* __restrict__ hr, int d, float eps) {
+    __shared__ float red[4];
+    float ss = 0.f;
+    for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(xr + i);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(xr + i + 4);
+        ss += a[0] * a[0] + a[1] * a[1] + a[2] * a[2] + a[3] * a[3];
+        ss += b[0] * b[0] + b[1] * b[1] + b[2] * b[2] + b[3] * b[3];
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    float tot = 0.f;
+    const int nw = blockDim.x >> 6;
+    for (int w = 0; w < nw; ++w) tot += red[w];
+    const float r = 1.f / sqrtf(tot / (float)d + eps);
+    for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(xr + i);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(xr + i + 4);
+        const u32x4 gg = *reinterpret_cast<const u32x4*>(g + i);
+        float gv[8];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            gv[2 * w] = __uint_as_float(gg[w] << 16);
+            gv[2 * w + 1] = __uint_as_float(gg[w] & 0xffff0000u);
+        }
+        u32x4 o;
+        o[0] = pack_bf16x2(a[0] * r * gv[0], a[1] * r * gv[1]);
+        o[1] = pack_bf16x2(a[2] * r * gv[2], a[3] * r * gv[3]);
+        o[2] = pack_bf16x2(b[0] * r * gv[4], b[1] * r * gv[5]);
+        o[3] = pack_bf16x2(b[2] * r * gv[6], b[3] * r * gv[7]);
+        *reinterpret_cast<u32x4*>(hr + i) = o;
+    }
+}
+
+__global__ void rmsnorm_kernel(const float* __restrict__ x, const bf16_t* __restrict__ g,
+                               bf16_t* __restrict__ h, int d, float eps) {
+    const int64_t r = blockIdx.x;
+    rmsnorm_row(x + r * d, g, h + r * d, d, eps);
+}
+
+__global__ void rmsnorm_draft_kernel(const float* __restrict__ x, const bf16_t* __restrict__ g,
+                                     bf16_t* __restrict__ h, int S, int P, int D, int d, float eps) {
+    const int r = blockIdx.x;
+    const int b = r / D, i = r - b * D;
+    rmsnorm_row(x + ((int64_t)b * S + P + i) * d, g, h + (int64_t)r * d, d, eps);
+}
+
+// Merge per-vocabulary-tile partials in tile order (deterministic).
+__global__ void lmhead_merge_kernel(const float4* __restrict__ part, int n_tiles, int R,
+                                    int32_t* __restrict__ top1, float* __restrict__ conf,
+                                    float* __restrict__ max_logit) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= R) return;
+    float m = -INFINITY;
+    int idx = 0x7fffffff;
+    for (int t = 0; t < n_tiles; ++t) {
+        const float4 p = part[(int64_t)t * R + r];
+        const int pi = __float_as_int(p.y);
+        if (p.x > m || (p.x == m && pi < idx)) {
+            m = p.x;
+            idx = pi;
+        }
+    }
+    float s = 0.f;
+    const float ml = m * kLog2e;
+    for (int t = 0; t < n_tiles; ++t) {
+        const float4 p = part[(int64_t)t * R + r];
+        if (p.z != 0.f) s += p.z * exp2f(p.x * kLog2e - ml);
+    }
+    top1[r] = idx;
+    conf[r] = 1.f / s;
+    if (max_logit) max_logit[r] = m;
+}
+
+// Threshold rule, all draft slots at once from the same forward pass.
+__global__ void edit_kernel(int32_t* __restrict__ tokens, int S, int P, int D,
+                            const int32_t* __restrict__ top1, const float* __restrict__ conf,
+                            float threshold, int mask_id, int32_t* __restrict__ counters,
+                            int32_t* __restrict__ out_top1, float* __restrict__ out_conf, int n) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    int unm = 0, edt = 0;
+    if (r < n) {
+        const int b = r / D, i = r - b * D;
+        int32_t* slot = tokens + (int64_t)b * S + P + i;
+        const int32_t cur = *slot;
+        const int32_t t = top1[r];
+        const float c = conf[r];
+        if (t != mask_id && c >= threshold && t != cur) {
+            *slot = t;
+            if (cur == mask_id) unm = 1; else edt = 1;
+        }
+        if (out_top1) out_top1[r] = t;
+        if (out_conf) out_conf[r] = c;
+    }
+    const unsigned long long bu = __ballot(unm), be = __ballot(edt);
+    if ((threadIdx.x & 63) == 0) {
+        if (bu) atomicAdd(&counters[0], (int)__popcll(bu));
+        if (be) atomicAdd(&counters[1], (int)__popcll(be));
+    }
+}
+
+__global__ void apply_mask_kernel(const int32_t* __restrict__ prompt, const int32_t* __restrict__ draft,
+                                  const uint8_t* __restrict__ mask, int32_t* __restrict__ tokens,
+                                  int P, int D, int mask_id, int n) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n) return;
+    const int S = P + D;
+    const int b = idx / S, s = idx - b * S;
+    int32_t v;
+    if (s < P) {
+        v = prompt[(int64_t)b * P + s];
+    } else {
+        const int64_t di = (int64_t)b * D + (s - P);
+        v = (mask && mask[di]) ? mask_id : draft[di];
+    }
+    tokens[idx] = v;
+}
+
+__global__ void copy_draft_out_kernel(const int32_t* __restrict__ tokens, int32_t* __restrict__ draft,
+                                      int S, int P, int D, int n) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    const int b = r / D, i = r - b * D;
+    draft[r] = tokens[(int64_t)b * S + P + i];
+}
+
+__global__ void count_masks_kernel(const int32_t* __restrict__ tokens, int S, int P, int D,
+                                   int mask_id, int32_t* __restrict__ counter, int n) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    int hit = 0;
+    if (r < n) {
+        const int b = r / D, i = r - b * D;
+        hit = tokens[(int64_t)b * S + P + i] == mask_id;
+    }
+    const unsigned long long bm = __ballot(hit);
+    if ((threadIdx.x & 63) == 0 && bm) atomicAdd(counter, (int)__popcll(bm));
+}
+
+__global__ void zero_i32_kernel(int32_t* __restrict__ p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+
+}  // namespace
+
+void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
+                  hipStream_t st) {
+    hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, st, tokens, emb, x, d, V);
+}
+
+void launch_rmsnorm(const float* x, const bf16_t* g, bf16_t* h, int rows, int d, float eps,
+                    hipStream_t st) {
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3(rows), dim3(256), 0, st, x, g, h, d, eps);
+}
+
+void launch_rmsnorm_draft_rows(const float* x, const bf16_t* g, bf16_t* h, int B, int S, int P,
+                               int D, int d, float eps, hipStream_t st) {
+    hipLaunchKernelGGL(rmsnorm_draft_kernel, dim3(B * D), dim3(256), 0, st, x, g, h, S, P, D, d, eps);
+}
+
+void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* top1, float* conf,
+                         float* max_logit, hipStream_t st) {
+    hipLaunchKernelGGL(lmhead_merge_kernel, dim3((R + 255) / 256), dim3(256), 0, st, partials,
+                       n_tiles, R, top1, conf, max_logit);
+}
+
+void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top1, const float* conf,
+                 float threshold, int mask_id, int32_t* counters, int32_t* out_top1,
+                 float* out_conf, hipStream_t st) {
+    const int n = B * D;
+    hipLaunchKernelGGL(edit_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, S, P, D, top1,
+                       conf, threshold, mask_id, counters, out_top1, out_conf, n);
+}
+
+void launch_apply_mask(const int32_t* prompt, const int32_t* draft, const uint8_t* mask,
+                       int32_t* tokens, int B, int P, int D, int mask_id, hipStream_t st) {
+    const int n = B * (P + D);
+    hipLaunchKernelGGL(apply_mask_kernel, dim3((n + 255) / 256), dim3(256), 0, st, prompt, draft,
+                       mask, tokens, P, D, mask_id, n);
+}
+
+void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, int P, int D,
+                           hipStream_t st) {
+    const int n = B * D;
+    hipLaunchKernelGGL(copy_draft_out_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, draft,
+                       S, P, D, n);
+}
+
+void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int mask_id,
+                        int32_t* counter, hipStream_t st) {
+    const int n = B * D;
+    hipLaunchKernelGGL(count_masks_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, S, P, D,
+                       mask_id, counter, n);
+}
+
+void launch_zero_i32(int32_t* p, int n, hipStream_t st) {
+    hipLaunchKernelGGL(zero_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
+}

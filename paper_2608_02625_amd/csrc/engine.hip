@@ -1,0 +1,712 @@
+// Host engine and C ABI of the refinement-step library (see include/dlm.h).
+//
+// The engine lays the synthetic weights out in the caller's device buffer,
+// carves the caller's workspace, and enqueues the kernel sequence of one
+// refinement pass on the caller's stream:
+//   embed -> L x [rmsnorm, QKV GEMM (+RoPE), attention, O GEMM (+residual),
+//                 rmsnorm, FFN (dense SwiGLU, or router/top-k/dispatch/grouped
+//                 expert GEMMs/combine)]
+//         -> final rmsnorm of draft rows -> LM-head GEMM with fused softmax
+//            partials -> merge -> threshold edit.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "../../include/dlm.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dlm_status fail(dlm_status s, const std::string& msg) {
+    g_last_error = msg;
+    return s;
+}
+
+#define HIP_TRY(expr)                                                                         \
+    do {                                                                                      \
+        hipError_t _e = (expr);                                                               \
+        if (_e != hipSuccess)                                                                 \
+            return fail(DLM_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(_e));     \
+    } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Tensor kinds (layer_field 0: embedding 0, LM head 1).
+enum { K_WQ = 0, K_WK, K_WV, K_WO, K_FG, K_FU, K_FD, K_ROUTER, K_EG, K_EU, K_ED, K_SG, K_SU, K_SD };
+
+uint32_t tensor_id(int layer_field, int kind, int expert) {
+    return ((uint32_t)layer_field << 20) | ((uint32_t)kind << 12) | (uint32_t)expert;
+}
+
+struct TensorInit {
+    size_t off;          // byte offset in the weight buffer
+    uint64_t n_phys;     // physical elements
+    uint32_t cols;
+    uint32_t tid_a, tid_b;
+    int layout;          // 0 plain, 1 gate/up interleaved in 32-row blocks
+    float scale;         // lm_head_scale for the LM head, else 1
+    int kind_fill;       // 1: fill with 1.0 (norm gains) instead of random
+};
+
+struct LayerPtrs {
+    size_t wqkv, wo, g1, g2, wgu, wd, wr;
+};
+
+struct WeightPlan {
+    size_t total = 0;
+    size_t emb = 0, lm = 0, gf = 0;
+    std::vector<LayerPtrs> layers;
+    std::vector<TensorInit> inits;
+};
+
+std::string validate(const dlm_config* c) {
+    if (!c) return "config is NULL";
+    if (c->n_layers < 0) return "n_layers < 0";
+    if (c->d_model <= 0 || c->d_model % 128) return "d_model must be a positive multiple of 128";
+    if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
+    if (c->n_heads <= 0 || c->n_kv_heads <= 0 || c->n_heads % c->n_kv_heads)
+        return "n_heads must be a positive multiple of n_kv_heads";
+    if ((c->n_heads * c->head_dim) % 128 || (c->n_kv_heads * c->head_dim) % 128)
+        return "n_heads*head_dim and n_kv_heads*head_dim must be multiples of 128";
+    if (c->vocab < 2) return "vocab must be >= 2";
+    if (c->mask_id < 0 || c->mask_id >= c->vocab) return "mask_id out of range";
+    if (c->n_experts < 0 || c->n_experts > 256) return "n_experts must be in [0, 256]";
+    if (c->n_experts == 0) {
+        if (c->ffn_dim <= 0 || c->ffn_dim % 64) return "ffn_dim must be a positive multiple of 64";
+    } else {
+        if (c->top_k < 1 || c->top_k > 8 || c->top_k > c->n_experts) return "top_k must be in [1, min(8, n_experts)]";
+        if (c->expert_ffn_dim <= 0 || c->expert_ffn_dim % 64) return "expert_ffn_dim must be a positive multiple of 64";
+        if (c->n_shared_experts < 0 || c->n_shared_experts > 1) return "n_shared_experts must be 0 or 1";
+    }
+    if (!(c->norm_eps >= 0.f) || !isfinite(c->norm_eps)) return "norm_eps must be finite and >= 0";
+    if (!(c->rope_theta > 0.f) || !isfinite(c->rope_theta)) return "rope_theta must be finite and > 0";
+    if (!isfinite(c->init_std) || !isfinite(c->lm_head_scale)) return "init_std / lm_head_scale must be finite";
+    return "";
+}
+
+WeightPlan plan_weights(const dlm_config& c) {
+    WeightPlan p;
+    const int d = c.d_model, hd = c.head_dim, H = c.n_heads, KV = c.n_kv_heads;
+    auto add = [&](uint64_t elems) {
+        const size_t off = p.total;
+        p.total = align_up(p.total + elems * 2);
+        return off;
+    };
+    auto plain = [&](size_t off, uint64_t rows, uint32_t cols, uint32_t tid, float scale) {
+        p.inits.push_back(TensorInit{off, rows * cols, cols, tid, tid, 0, scale, 0});
+    };
+    auto inter = [&](size_t off, uint64_t f, uint32_t cols, uint32_t tg, uint32_t tu) {
+        p.inits.push_back(TensorInit{off, 2 * f * cols, cols, tg, tu, 1, 1.f, 0});
+    };
+    auto ones = [&](size_t off, uint64_t n) {
+        p.inits.push_back(TensorInit{off, n, (uint32_t)n, 0, 0, 0, 1.f, 1});
+    };
+    p.emb = add((uint64_t)c.vocab * d);
+    plain(p.emb, c.vocab, d, tensor_id(0, 0, 0), 1.f);
+    p.lm = add((uint64_t)c.vocab * d);
+    plain(p.lm, c.vocab, d, tensor_id(0, 1, 0), c.lm_head_scale);
+    p.gf = add(d);
+    ones(p.gf, d);
+    for (int l = 0; l < c.n_layers; ++l) {
+        const int f = l + 1;
+        LayerPtrs L{};
+        const uint64_t nq = (uint64_t)H * hd, nk = (uint64_t)KV * hd;
+        L.wqkv = add((nq + 2 * nk) * d);
+        plain(L.wqkv, nq, d, tensor_id(f, K_WQ, 0), 1.f);
+        plain(L.wqkv + nq * d * 2, nk, d, tensor_id(f, K_WK, 0), 1.f);
+        plain(L.wqkv + (nq + nk) * d * 2, nk, d, tensor_id(f, K_WV, 0), 1.f);
+        L.wo = add((uint64_t)d * nq);
+        plain(L.wo, d, (uint32_t)nq, tensor_id(f, K_WO, 0), 1.f);
+        L.g1 = add(d);
+        ones(L.g1, d);
+        L.g2 = add(d);
+        ones(L.g2, d);
+        if (c.n_experts == 0) {
+            const uint64_t F = c.ffn_dim;
+            L.wgu = add(2 * F * d);
+            inter(L.wgu, F, d, tensor_id(f, K_FG, 0), tensor_id(f, K_FU, 0));
+            L.wd = add((uint64_t)d * F);
+            plain(L.wd, d, (uint32_t)F, tensor_id(f, K_FD, 0), 1.f);
+            L.wr = 0;
+        } else {
+            const uint64_t F = c.expert_ffn_dim;
+            const int G = c.n_experts + c.n_shared_experts;
+            L.wr = add((uint64_t)c.n_experts * d);
+            plain(L.wr, c.n_experts, d, tensor_id(f, K_ROUTER, 0), 1.f);
+            L.wgu = add((uint64_t)G * 2 * F * d);
+            for (int e = 0; e < G; ++e) {
+                const bool sh = e >= c.n_experts;
+                const int ei = sh ? e - c.n_experts : e;
+                inter(L.wgu + (uint64_t)e * 2 * F * d * 2, F, d, tensor_id(f, sh ? K_SG : K_EG, ei),
+                      tensor_id(f, sh ? K_SU : K_EU, ei));
+            }
+            L.wd = add((uint64_t)G * d * F);
+            for (int e = 0; e < G; ++e) {
+                const bool sh = e >= c.n_experts;
+                const int ei = sh ? e - c.n_experts : e;
+                plain(L.wd + (uint64_t)e * d * F * 2, d, (uint32_t)F, tensor_id(f, sh ? K_SD : K_ED, ei), 1.f);
+            }
+        }
+        p.layers.push_back(L);
+    }
+    return p;
+}
+
+// Workspace carve-up for one (B, P, D).
+struct Workspace {
+    size_t total = 0;
+    size_t x, h, q, k, vt, attn, rope, hf, logits, ids, wts, counts, cursor, grp_off, tile_tab,
+        n_tiles, slot, a_rows, hexp, y, hfin, partials, top1, conf, maxlogit, counters, tokens;
+    int rows_total = 0, max_tiles = 0, n_vtiles = 0;
+};
+
+constexpr int kExpertBM = 256, kExpertBN = 256;
+constexpr int kHeadBM = 256, kHeadBN = 256;
+
+Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
+    Workspace w;
+    const int64_t S = P + D, T = (int64_t)B * S, R = (int64_t)B * D;
+    const int64_t S_pad = (S + 63) / 64 * 64;
+    const int d = c.d_model, hd = c.head_dim;
+    auto add = [&](int64_t bytes) {
+        const size_t off = w.total;
+        w.total = align_up(w.total + (size_t)std::max<int64_t>(bytes, 1));
+        return off;
+    };
+    w.x = add(T * d * 4);
+    w.h = add(T * d * 2);
+    w.q = add((int64_t)B * c.n_heads * S * hd * 2);
+    w.k = add((int64_t)B * c.n_kv_heads * S * hd * 2);
+    w.vt = add((int64_t)B * c.n_kv_heads * hd * S_pad * 2);
+    w.attn = add(T * c.n_heads * hd * 2);
+    w.rope = add(S * (hd / 2) * 8);
+    if (c.n_experts == 0) {
+        w.hf = add(T * c.ffn_dim * 2);
+    } else {
+        const int E = c.n_experts, k = c.top_k, G = E + c.n_shared_experts;
+        w.rows_total = (int)(T * k + T * c.n_shared_experts);
+        w.max_tiles = (w.rows_total + kExpertBM - 1) / kExpertBM + G;
+        w.logits = add(T * E * 4);
+        w.ids = add(T * k * 4);
+        w.wts = add(T * k * 4);
+        w.counts = add(E * 4);
+        w.cursor = add(G * 4);
+        w.grp_off = add((G + 1) * 4);
+        w.tile_tab = add((int64_t)w.max_tiles * 8);
+        w.n_tiles = add(4);
+        w.slot = add(T * k * 4);
+        w.a_rows = add((int64_t)w.rows_total * 4);
+        w.hexp = add((int64_t)w.rows_total * c.expert_ffn_dim * 2);
+        w.y = add((int64_t)w.rows_total * d * 2);
+    }
+    w.n_vtiles = (c.vocab + kHeadBM - 1) / kHeadBM;
+    w.hfin = add(R * d * 2);
+    w.partials = add((int64_t)w.n_vtiles * R * 16);
+    w.top1 = add(R * 4);
+    w.conf = add(R * 4);
+    w.maxlogit = add(R * 4);
+    w.counters = add(sizeof(dlm_stats));
+    w.tokens = add(T * 4);
+    return w;
+}
+
+std::string check_shape(int B, int P, int D) {
+    if (B <= 0) return "batch must be > 0";
+    if (P < 0) return "prompt_len must be >= 0";
+    if (D <= 0) return "draft_len must be > 0";
+    const int64_t S = (int64_t)P + D;
+    if (S > 65536 || (int64_t)B * S > (1 << 26)) return "batch * seq_len too large";
+    return "";
+}
+
+struct ProfRec {
+    const char* name;
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct dlm_model {
+    dlm_config cfg;
+    uint64_t seed;
+    char* base;
+    size_t bytes;
+    WeightPlan plan;
+    // profiling
+    std::string prof_filter;
+    bool prof_on = false;
+    std::vector<ProfRec> prof;
+    size_t prof_used = 0;
+};
+
+namespace {
+
+struct Ctx {
+    dlm_model* m;
+    const dlm_config& c;
+    char* ws;
+    Workspace w;
+    hipStream_t st;
+    int B, P, D, S, T, R;
+    template <class Tp>
+    Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
+    const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
+};
+
+// Profiling: HIP events around launches of kernels whose name matches the filter.
+void prof_begin(Ctx& x, const char* name) {
+    dlm_model* m = x.m;
+    if (!m->prof_on) return;
+    if (!(m->prof_filter == "*" || m->prof_filter == name)) return;
+    if (m->prof_used == m->prof.size()) {
+        ProfRec r{name, nullptr, nullptr};
+        if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return;
+        m->prof.push_back(r);
+    }
+    ProfRec& r = m->prof[m->prof_used];
+    r.name = name;
+    hipEventRecord(r.a, x.st);
+}
+void prof_end(Ctx& x, const char* name) {
+    dlm_model* m = x.m;
+    if (!m->prof_on) return;
+    if (!(m->prof_filter == "*" || m->prof_filter == name)) return;
+    if (m->prof_used >= m->prof.size()) return;
+    hipEventRecord(m->prof[m->prof_used].b, x.st);
+    ++m->prof_used;
+}
+
+#define LAUNCH(ctx, name, call)          \
+    do {                                 \
+        prof_begin(ctx, name);           \
+        call;                            \
+        prof_end(ctx, name);             \
+    } while (0)
+
+dlm_status gemm(Ctx& x, const char* name, const GemmArgs& a, int epi, bool grouped, int bm, int bn,
+                int max_tiles) {
+    hipError_t e;
+    prof_begin(x, name);
+    e = launch_gemm(a, epi, grouped, bm, bn, max_tiles, x.st);
+    prof_end(x, name);
+    if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("gemm ") + name + ": " + hipGetErrorString(e));
+    return DLM_OK;
+}
+
+GemmArgs gemm_args(const bf16_t* A, int64_t lda, const bf16_t* B, int64_t ldb, int M, int N, int K) {
+    GemmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.A = A;
+    a.lda = lda;
+    a.B = B;
+    a.ldb = ldb;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.group_m = 4;
+    return a;
+}
+
+#define TRY(expr)                        \
+    do {                                 \
+        dlm_status _s = (expr);          \
+        if (_s != DLM_OK) return _s;     \
+    } while (0)
+
+// One transformer block on the fp32 residual stream x (in place).
+dlm_status run_layer(Ctx& x, int l) {
+    const dlm_config& c = x.c;
+    const LayerPtrs& L = x.m->plan.layers[l];
+    const int d = c.d_model, hd = c.head_dim, H = c.n_heads, KV = c.n_kv_heads;
+    float* xs = x.at<float>(x.w.x);
+    bf16_t* h = x.at<bf16_t>(x.w.h);
+    bf16_t* q = x.at<bf16_t>(x.w.q);
+    bf16_t* k = x.at<bf16_t>(x.w.k);
+    bf16_t* vt = x.at<bf16_t>(x.w.vt);
+    bf16_t* attn = x.at<bf16_t>(x.w.attn);
+
+    LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g1), h, x.T, d, c.norm_eps, x.st));
+    {
+        const int N = (H + 2 * KV) * hd;
+        GemmArgs a = gemm_args(h, d, x.wt(L.wqkv), d, x.T, N, d);
+        a.q = q;
+        a.k = k;
+        a.vt = vt;
+        a.rope = x.at<float2>(x.w.rope);
+        a.seq = x.S;
+        a.seq_pad = (x.S + 63) / 64 * 64;
+        a.n_heads = H;
+        a.n_kv = KV;
+        a.head_dim = hd;
+        TRY(gemm(x, "gemm_qkv", a, EPI_QKV, false, x.T >= 4096 ? 256 : 128, 256, 0));
+    }
+    {
+        prof_begin(x, "attention");
+        hipError_t e = launch_attention(q, k, vt, attn, x.B, x.S, H, KV, hd, x.st);
+        prof_end(x, "attention");
+        if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("attention: ") + hipGetErrorString(e));
+    }
+    {
+        GemmArgs a = gemm_args(attn, (int64_t)H * hd, x.wt(L.wo), (int64_t)H * hd, x.T, d, H * hd);
+        a.out = xs;
+        a.ldo = d;
+        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, x.T >= 4096 ? 256 : 128, 128, 0));
+    }
+    LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g2), h, x.T, d, c.norm_eps, x.st));
+    if (c.n_experts == 0) {
+        const int F = c.ffn_dim;
+        bf16_t* hf = x.at<bf16_t>(x.w.hf);
+        GemmArgs a = gemm_args(h, d, x.wt(L.wgu), d, x.T, 2 * F, d);
+        a.out = hf;
+        a.ldo = F;
+        TRY(gemm(x, "gemm_ffn_gate_up", a, EPI_SWIGLU, false, x.T >= 4096 ? 256 : 128, 256, 0));
+        GemmArgs b = gemm_args(hf, F, x.wt(L.wd), F, x.T, d, F);
+        b.out = xs;
+        b.ldo = d;
+        TRY(gemm(x, "gemm_ffn_down", b, EPI_RESID, false, x.T >= 4096 ? 256 : 128, 128, 0));
+        return DLM_OK;
+    }
+    const int E = c.n_experts, kk = c.top_k, NS = c.n_shared_experts, F = c.expert_ffn_dim;
+    float* logits = x.at<float>(x.w.logits);
+    int32_t* ids = x.at<int32_t>(x.w.ids);
+    float* wts = x.at<float>(x.w.wts);
+    int32_t* counts = x.at<int32_t>(x.w.counts);
+    int32_t* cursor = x.at<int32_t>(x.w.cursor);
+    int32_t* grp_off = x.at<int32_t>(x.w.grp_off);
+    int2* tile_tab = x.at<int2>(x.w.tile_tab);
+    int32_t* n_tiles = x.at<int32_t>(x.w.n_tiles);
+    int32_t* slot = x.at<int32_t>(x.w.slot);
+    int32_t* a_rows = x.at<int32_t>(x.w.a_rows);
+    bf16_t* hexp = x.at<bf16_t>(x.w.hexp);
+    bf16_t* y = x.at<bf16_t>(x.w.y);
+    {
+        GemmArgs a = gemm_args(h, d, x.wt(L.wr), d, x.T, E, d);
+        a.out = logits;
+        a.ldo = E;
+        TRY(gemm(x, "gemm_router", a, EPI_F32, false, 128, 64, 0));
+    }
+    LAUNCH(x, "topk", launch_topk(logits, x.T, E, kk, ids, wts, counts, x.st));
+    LAUNCH(x, "dispatch_scan",
+           launch_dispatch_scan(counts, E, NS, x.T, kExpertBM, grp_off, tile_tab, n_tiles, cursor, x.st));
+    LAUNCH(x, "dispatch_scatter",
+           launch_dispatch_scatter(ids, x.T, kk, E, NS, grp_off, cursor, slot, a_rows, x.st));
+    {
+        GemmArgs a = gemm_args(h, d, x.wt(L.wgu), d, 0, 2 * F, d);
+        a.b_group_stride = (int64_t)2 * F * d;
+        a.tile_tab = tile_tab;
+        a.n_tiles = n_tiles;
+        a.grp_off = grp_off;
+        a.a_rows = a_rows;
+        a.out = hexp;
+        a.ldo = F;
+        TRY(gemm(x, "gemm_expert_gate_up", a, EPI_SWIGLU, true, kExpertBM, kExpertBN, x.w.max_tiles));
+    }
+    {
+        GemmArgs a = gemm_args(hexp, F, x.wt(L.wd), F, 0, d, F);
+        a.b_group_stride = (int64_t)d * F;
+        a.tile_tab = tile_tab;
+        a.n_tiles = n_tiles;
+        a.grp_off = grp_off;
+        a.a_rows = nullptr;
+        a.out = y;
+        a.ldo = d;
+        TRY(gemm(x, "gemm_expert_down", a, EPI_BF16, true, kExpertBM, kExpertBN, x.w.max_tiles));
+    }
+    LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d, x.st));
+    return DLM_OK;
+}
+
+dlm_status run_prologue(Ctx& x, const int32_t* tokens) {
+    const dlm_config& c = x.c;
+    LAUNCH(x, "rope_table", launch_rope_table(x.at<float2>(x.w.rope), x.S, c.head_dim / 2, (double)c.rope_theta, x.st));
+    if (c.n_experts > 0) LAUNCH(x, "zero", launch_zero_i32(x.at<int32_t>(x.w.counts), c.n_experts, x.st));
+    if (tokens) LAUNCH(x, "embed", launch_embed(tokens, x.wt(x.m->plan.emb), x.at<float>(x.w.x), x.T, c.d_model, c.vocab, x.st));
+    return DLM_OK;
+}
+
+// Final norm of the draft rows, LM head with fused softmax partials, merge.
+dlm_status run_head(Ctx& x, int32_t* top1, float* conf, float* maxlogit, float* logits_out) {
+    const dlm_config& c = x.c;
+    bf16_t* hfin = x.at<bf16_t>(x.w.hfin);
+    LAUNCH(x, "rmsnorm_final", launch_rmsnorm_draft_rows(x.at<float>(x.w.x), x.wt(x.m->plan.gf), hfin, x.B,
+                                                         x.S, x.P, x.D, c.d_model, c.norm_eps, x.st));
+    GemmArgs a = gemm_args(x.wt(x.m->plan.lm), c.d_model, hfin, c.d_model, c.vocab, x.R, c.d_model);
+    a.partials = x.at<float4>(x.w.partials);
+    a.group_m = 4;
+    TRY(gemm(x, "gemm_lm_head", a, EPI_LMHEAD, false, kHeadBM, kHeadBN, 0));
+    LAUNCH(x, "lmhead_merge", launch_lmhead_merge(a.partials, x.w.n_vtiles, x.R, top1, conf, maxlogit, x.st));
+    if (logits_out) {
+        GemmArgs b = gemm_args(x.wt(x.m->plan.lm), c.d_model, hfin, c.d_model, c.vocab, x.R, c.d_model);
+        b.out = logits_out;
+        b.ldo = c.vocab;
+        TRY(gemm(x, "gemm_logits_debug", b, EPI_F32_T, false, 256, 256, 0));
+    }
+    return DLM_OK;
+}
+
+dlm_status check_common(dlm_model* m, int B, int P, int D, void* ws, size_t ws_bytes, Workspace* w) {
+    if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+    std::string e = check_shape(B, P, D);
+    if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
+    *w = plan_workspace(m->cfg, B, P, D);
+    if (!ws) return fail(DLM_ERR_INVALID_ARG, "workspace is NULL");
+    if (ws_bytes < w->total)
+        return fail(DLM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(w->total) + " bytes, got " +
+                                           std::to_string(ws_bytes));
+    if (((uintptr_t)ws) % kAlign) return fail(DLM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    return DLM_OK;
+}
+
+Ctx ctx_for(dlm_model* m, int B, int P, int D, void* ws, const Workspace& w, void* stream) {
+    Ctx x{m, m->cfg, (char*)ws, w, (hipStream_t)stream, B, P, D, P + D, B * (P + D), B * D};
+    return x;
+}
+
+dlm_status step_impl(Ctx& x, int32_t* tokens, float threshold, int32_t* top1_out, float* conf_out,
+                     dlm_stats* stats_out) {
+    const dlm_config& c = x.c;
+    int32_t* counters = x.at<int32_t>(x.w.counters);
+    LAUNCH(x, "zero", launch_zero_i32(counters, 4, x.st));
+    TRY(run_prologue(x, tokens));
+    for (int l = 0; l < c.n_layers; ++l) TRY(run_layer(x, l));
+    TRY(run_head(x, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf), x.at<float>(x.w.maxlogit), nullptr));
+    LAUNCH(x, "edit", launch_edit(tokens, x.B, x.S, x.P, x.D, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf),
+                                  threshold, c.mask_id, counters, top1_out, conf_out, x.st));
+    if (stats_out) HIP_TRY(hipMemcpyAsync(stats_out, counters, sizeof(dlm_stats), hipMemcpyDeviceToDevice, x.st));
+    return DLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dlm_last_error(void) { return g_last_error.c_str(); }
+
+size_t dlm_weights_bytes(const dlm_config* cfg) {
+    if (!validate(cfg).empty()) return 0;
+    return plan_weights(*cfg).total;
+}
+
+size_t dlm_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len) {
+    if (!validate(cfg).empty() || !check_shape(batch, prompt_len, draft_len).empty()) return 0;
+    return plan_workspace(*cfg, batch, prompt_len, draft_len).total;
+}
+
+dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void* d_weights,
+                                      size_t weights_bytes, void* hip_stream, dlm_model** out) {
+    const std::string e = validate(cfg);
+    if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
+    if (!out) return fail(DLM_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (!d_weights) return fail(DLM_ERR_INVALID_ARG, "weights buffer is NULL");
+    if (((uintptr_t)d_weights) % kAlign) return fail(DLM_ERR_INVALID_ARG, "weights buffer must be 256-byte aligned");
+    WeightPlan plan = plan_weights(*cfg);
+    if (weights_bytes < plan.total)
+        return fail(DLM_ERR_WORKSPACE, "weights buffer too small: need " + std::to_string(plan.total) + " bytes");
+    hipStream_t st = (hipStream_t)hip_stream;
+    char* base = (char*)d_weights;
+    for (const TensorInit& t : plan.inits) {
+        bf16_t* dst = reinterpret_cast<bf16_t*>(base + t.off);
+        if (t.kind_fill) {
+            launch_fill_bf16(dst, t.n_phys, (bf16_t)0x3f80, st);
+        } else {
+            const float c = (float)((double)cfg->init_std * (double)t.scale * sqrt(3.0) / 65536.0);
+            launch_init_weights(dst, t.n_phys, t.cols, t.tid_a, t.tid_b, t.layout, seed, c, st);
+        }
+        HIP_TRY(hipGetLastError());
+    }
+    dlm_model* m = new dlm_model();
+    m->cfg = *cfg;
+    m->seed = seed;
+    m->base = base;
+    m->bytes = weights_bytes;
+    m->plan = std::move(plan);
+    *out = m;
+    return DLM_OK;
+}
+
+dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                           int32_t* d_tokens, float threshold, void* d_workspace, size_t workspace_bytes,
+                           void* hip_stream, int32_t* d_top1, float* d_conf, dlm_stats* d_stats) {
+    Workspace w;
+    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    m->prof_used = 0;
+    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+    return step_impl(x, d_tokens, threshold, d_top1, d_conf, d_stats);
+}
+
+dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                      const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
+                      float threshold, void* d_workspace, size_t workspace_bytes, void* hip_stream,
+                      dlm_stats* h_stats) {
+    Workspace w;
+    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+    if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
+    if (n_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_steps < 0");
+    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    m->prof_used = 0;
+    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+    int32_t* tokens = x.at<int32_t>(w.tokens);
+    int32_t* counters = x.at<int32_t>(w.counters);
+    launch_apply_mask(d_prompt, d_draft, d_mask, tokens, batch, prompt_len, draft_len, m->cfg.mask_id, x.st);
+    HIP_TRY(hipGetLastError());
+    dlm_stats tot{0, 0, 0, 0};
+    for (int s = 0; s < n_steps; ++s) {
+        TRY(step_impl(x, tokens, threshold, nullptr, nullptr, nullptr));
+        dlm_stats st{};
+        HIP_TRY(hipMemcpyAsync(&st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
+        HIP_TRY(hipStreamSynchronize(x.st));
+        tot.n_unmasked += st.n_unmasked;
+        tot.n_edited += st.n_edited;
+        tot.steps_run += 1;
+        if (st.n_unmasked + st.n_edited == 0) break;
+    }
+    launch_copy_draft_out(tokens, d_draft, batch, x.S, prompt_len, draft_len, x.st);
+    launch_zero_i32(counters, 4, x.st);
+    launch_count_masks(tokens, batch, x.S, prompt_len, draft_len, m->cfg.mask_id, counters + 2, x.st);
+    HIP_TRY(hipGetLastError());
+    dlm_stats st{};
+    HIP_TRY(hipMemcpyAsync(&st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
+    HIP_TRY(hipStreamSynchronize(x.st));
+    tot.n_masked_left = st.n_masked_left;
+    if (h_stats) *h_stats = tot;
+    return DLM_OK;
+}
+
+dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                             const int32_t* d_tokens, void* d_workspace, size_t workspace_bytes,
+                             void* hip_stream, float* d_hidden, float* d_max_logit, int32_t* d_top1,
+                             float* d_conf, float* d_logits) {
+    Workspace w;
+    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+    TRY(run_prologue(x, d_tokens));
+    for (int l = 0; l < m->cfg.n_layers; ++l) TRY(run_layer(x, l));
+    if (d_hidden)
+        HIP_TRY(hipMemcpyAsync(d_hidden, x.at<float>(w.x), (size_t)x.T * m->cfg.d_model * 4,
+                               hipMemcpyDeviceToDevice, x.st));
+    if (d_max_logit || d_top1 || d_conf || d_logits) {
+        TRY(run_head(x, x.at<int32_t>(w.top1), x.at<float>(w.conf), x.at<float>(w.maxlogit), d_logits));
+        const size_t R = (size_t)x.R;
+        if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
+        if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
+        if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
+    }
+    return DLM_OK;
+}
+
+dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len, const float* d_x_in,
+                           float* d_x_out, void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+    Workspace w;
+    TRY(check_common(m, batch, 0, seq_len, d_workspace, workspace_bytes, &w));
+    if (layer < 0 || layer >= m->cfg.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
+    if (!d_x_in || !d_x_out) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
+    Ctx x = ctx_for(m, batch, 0, seq_len, d_workspace, w, hip_stream);
+    const size_t bytes = (size_t)x.T * m->cfg.d_model * 4;
+    HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x_in, bytes, hipMemcpyDeviceToDevice, x.st));
+    TRY(run_prologue(x, nullptr));
+    TRY(run_layer(x, layer));
+    HIP_TRY(hipMemcpyAsync(d_x_out, x.at<float>(w.x), bytes, hipMemcpyDeviceToDevice, x.st));
+    return DLM_OK;
+}
+
+dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, const float* d_x,
+                          void* d_workspace, size_t workspace_bytes, void* hip_stream, float* d_max_logit,
+                          int32_t* d_top1, float* d_conf) {
+    Workspace w;
+    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+    if (!d_x) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
+    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+    HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x, (size_t)x.T * m->cfg.d_model * 4, hipMemcpyDeviceToDevice, x.st));
+    TRY(run_head(x, x.at<int32_t>(w.top1), x.at<float>(w.conf), x.at<float>(w.maxlogit), nullptr));
+    const size_t R = (size_t)x.R;
+    if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
+    if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
+    if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
+    return DLM_OK;
+}
+
+dlm_status dlm_weight_info(dlm_model* m, int32_t layer_field, int32_t kind, int32_t expert, void** d_ptr,
+                           int32_t* layout) {
+    if (!m || !d_ptr || !layout) return fail(DLM_ERR_INVALID_ARG, "NULL argument");
+    const dlm_config& c = m->cfg;
+    const size_t d = c.d_model;
+    if (layer_field == 0) {
+        if (kind == 0) { *d_ptr = m->base + m->plan.emb; *layout = 0; return DLM_OK; }
+        if (kind == 1) { *d_ptr = m->base + m->plan.lm; *layout = 0; return DLM_OK; }
+        return fail(DLM_ERR_INVALID_ARG, "unknown global tensor kind");
+    }
+    const int l = layer_field - 1;
+    if (l < 0 || l >= c.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
+    const LayerPtrs& L = m->plan.layers[l];
+    const size_t nq = (size_t)c.n_heads * c.head_dim, nk = (size_t)c.n_kv_heads * c.head_dim;
+    char* b = m->base;
+    *layout = 0;
+    switch (kind) {
+        case K_WQ: *d_ptr = b + L.wqkv; return DLM_OK;
+        case K_WK: *d_ptr = b + L.wqkv + nq * d * 2; return DLM_OK;
+        case K_WV: *d_ptr = b + L.wqkv + (nq + nk) * d * 2; return DLM_OK;
+        case K_WO: *d_ptr = b + L.wo; return DLM_OK;
+        default: break;
+    }
+    if (c.n_experts == 0) {
+        if (kind == K_FG || kind == K_FU) { *d_ptr = b + L.wgu; *layout = 1; return DLM_OK; }
+        if (kind == K_FD) { *d_ptr = b + L.wd; return DLM_OK; }
+        return fail(DLM_ERR_INVALID_ARG, "unknown dense-layer tensor kind");
+    }
+    const size_t F = c.expert_ffn_dim;
+    int e = expert;
+    if (kind == K_ROUTER) { *d_ptr = b + L.wr; return DLM_OK; }
+    if (kind >= K_SG && kind <= K_SD) {
+        if (expert < 0 || expert >= c.n_shared_experts) return fail(DLM_ERR_INVALID_ARG, "shared expert out of range");
+        e = c.n_experts + expert;
+        kind -= 3;
+    } else if (expert < 0 || expert >= c.n_experts) {
+        return fail(DLM_ERR_INVALID_ARG, "expert out of range");
+    }
+    if (kind == K_EG || kind == K_EU) { *d_ptr = b + L.wgu + (size_t)e * 2 * F * d * 2; *layout = 1; return DLM_OK; }
+    if (kind == K_ED) { *d_ptr = b + L.wd + (size_t)e * d * F * 2; return DLM_OK; }
+    return fail(DLM_ERR_INVALID_ARG, "unknown tensor kind");
+}
+
+dlm_status dlm_set_profiling(dlm_model* m, const char* name_filter) {
+    if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+    m->prof_on = name_filter != nullptr;
+    m->prof_filter = name_filter ? name_filter : "";
+    m->prof_used = 0;
+    return DLM_OK;
+}
+
+int32_t dlm_profile_read(dlm_model* m, const char** names, float* ms, int32_t max_entries) {
+    if (!m) return -1;
+    int32_t n = 0;
+    for (size_t i = 0; i < m->prof_used && n < max_entries; ++i) {
+        float t = 0.f;
+        if (hipEventSynchronize(m->prof[i].b) != hipSuccess) return -1;
+        if (hipEventElapsedTime(&t, m->prof[i].a, m->prof[i].b) != hipSuccess) return -1;
+        if (names) names[n] = m->prof[i].name;
+        if (ms) ms[n] = t;
+        ++n;
+    }
+    return n;
+}
+
+void dlm_free(dlm_model* m) {
+    if (!m) return;
+    for (ProfRec& r : m->prof) {
+        if (r.a) hipEventDestroy(r.a);
+        if (r.b) hipEventDestroy(r.b);
+    }
+    delete m;
+}
+
+}  // extern "C"

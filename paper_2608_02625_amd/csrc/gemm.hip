@@ -1,0 +1,359 @@
+// bf16 MFMA GEMM for gfx950 with fused epilogues.
+//
+// C[M x N] = A[M x K] * B[N x K]^T, fp32 accumulation, both operands K-contiguous.
+// A workgroup of 256 threads (4 waves in a 2x2 grid) owns a BM x BN tile; each
+// wave owns (BM/2) x (BN/2) as a grid of 32x32 accumulators fed by
+// v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through two LDS stages
+// (register-staged global loads for stage k+1 overlap the MFMAs of stage k).
+// LDS rows are 128 bytes (64 bf16) with 16-byte chunks XOR-swizzled by row
+// bits so that fragment reads of 32 consecutive rows spread over all banks.
+//
+// Grouped mode runs one GEMM per expert over a device-built tile table; the A
+// rows of a group may be gathered through an index array (token -> expert
+// rows), so the routed activations are never copied.
+//
+// Workgroup ids are remapped so that each of the 8 XCDs (which receive
+// workgroups round-robin) processes a contiguous range of tiles; within that
+// range dense GEMMs raster group_m row-tiles at a time to keep operands in L2.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int BM, int BN>
+struct TileCfg {
+    static constexpr int WM = BM / 2, WN = BN / 2;
+    static constexpr int TM = WM / 32, TN = WN / 32;
+    static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
+    static constexpr int STAGE = A_BYTES + B_BYTES;
+    static constexpr int LDS = 2 * STAGE;
+    static constexpr int A_PASSES = BM / 32, B_PASSES = BN / 32;
+};
+
+__device__ __forceinline__ int swz(int row, int chunk) {
+    return row * 128 + ((chunk ^ ((row & 7) ^ ((row >> 3) & 1))) << 4);
+}
+
+// QKV projection epilogue: RoPE (rotate-half) on the q and k columns, then
+// scatter to Q [B][H][S][hd], K [B][KV][S][hd] and V^T [B][KV][hd][seq_pad].
+// A wave's column range covers whole heads, so the rotation partners
+// (i, i + hd/2) sit in the same lane, subtiles j and j + hd/64.
+template <int TM, int TN, int HD>
+__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0,
+                                             int rows, int n0, int lrow0, int lcol0) {
+    constexpr int HALF = HD / 2, SPT = HD / 32, POFF = HD / 64;
+    const int Hq = a.n_heads * HD, Hk = a.n_kv * HD;
+    const int S = a.seq;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int row = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+            if (row >= rows) continue;
+            const int b = row / S, s = row - b * S;
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int c = n0 + lcol0 + j * 32;
+                if (c >= a.N) continue;
+                if (c < Hq + Hk) {
+                    if ((j % SPT) < POFF && j + POFF < TN) {
+                        const int hi = c % HD;            // < HALF
+                        const float2 cs = a.rope[s * HALF + hi];
+                        const float x1 = acc[i][j][e], x2 = acc[i][(j + POFF) % TN][e];
+                        const float o1 = x1 * cs.x - x2 * cs.y;
+                        const float o2 = x2 * cs.x + x1 * cs.y;
+                        bf16_t* dst;
+                        if (c < Hq)
+                            dst = a.q + (((int64_t)b * a.n_heads + c / HD) * S + s) * HD;
+                        else
+                            dst = a.k + (((int64_t)b * a.n_kv + (c - Hq) / HD) * S + s) * HD;
+                        dst[hi] = f32_to_bf16(o1);
+                        dst[hi + HALF] = f32_to_bf16(o2);
+                    }
+                } else {
+                    const int cv = c - Hq - Hk;
+                    const int kh = cv / HD, hi = cv - kh * HD;
+                    a.vt[(((int64_t)b * a.n_kv + kh) * HD + hi) * a.seq_pad + s] = f32_to_bf16(acc[i][j][e]);
+                }
+            }
+        }
+}
+
+template <int BM, int BN, int EPI, bool GROUPED>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
+    using T = TileCfg<BM, BN>;
+    __shared__ __attribute__((aligned(16))) char smem[T::LDS];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int tiles_n = (a.N + BN - 1) / BN;
+
+    // ---------------------------------------------------------------- tile decode
+    const int tiles_m_or_listed = GROUPED ? *a.n_tiles : (a.M + BM - 1) / BM;
+    const int total = tiles_m_or_listed * tiles_n;
+    const int chunk = (total + 7) >> 3;
+    const int w = blockIdx.x;
+    const int local = w >> 3;
+    if (local >= chunk) return;
+    const int L = (w & 7) * chunk + local;
+    if (L >= total) return;
+    int ti, tn;
+    if (GROUPED || a.group_m <= 1) {
+        ti = L / tiles_n;
+        tn = L - ti * tiles_n;
+    } else {
+        const int tiles_m = tiles_m_or_listed;
+        const int per_group = a.group_m * tiles_n;
+        const int grp = L / per_group;
+        const int first_m = grp * a.group_m;
+        const int gsz = min(tiles_m - first_m, a.group_m);
+        const int r = L - grp * per_group;
+        ti = first_m + r % gsz;
+        tn = r / gsz;
+    }
+    int g = 0, m0, row_base = 0, rows;
+    if (GROUPED) {
+        const int2 t = a.tile_tab[ti];
+        g = t.x;
+        m0 = t.y;
+        row_base = a.grp_off[g];
+        rows = a.grp_off[g + 1] - row_base;
+    } else {
+        m0 = ti * BM;
+        rows = a.M;
+    }
+    const int n0 = tn * BN;
+    const bf16_t* Bg = a.B + (GROUPED ? (int64_t)g * a.b_group_stride : 0);
+
+    // ---------------------------------------------------------------- main loop
+    const int lc = tid & 7, lr = tid >> 3;
+    const bf16_t* a_ptr[T::A_PASSES];
+    const bf16_t* b_ptr[T::B_PASSES];
+#pragma unroll
+    for (int p = 0; p < T::A_PASSES; ++p) {
+        const int r = min(m0 + lr + 32 * p, rows - 1);
+        int64_t grow = r;
+        if (GROUPED) grow = a.a_rows ? a.a_rows[row_base + r] : row_base + r;
+        a_ptr[p] = a.A + grow * a.lda + lc * 8;
+    }
+#pragma unroll
+    for (int p = 0; p < T::B_PASSES; ++p) {
+        const int n = min(n0 + lr + 32 * p, a.N - 1);
+        b_ptr[p] = Bg + (int64_t)n * a.ldb + lc * 8;
+    }
+
+    u32x4 ra[T::A_PASSES], rb[T::B_PASSES];
+    f32x16 acc[T::TM][T::TN];
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int p = 0; p < T::A_PASSES; ++p) ra[p] = *reinterpret_cast<const u32x4*>(a_ptr[p] + k0);
+#pragma unroll
+        for (int p = 0; p < T::B_PASSES; ++p) rb[p] = *reinterpret_cast<const u32x4*>(b_ptr[p] + k0);
+    };
+    auto lstore = [&](int buf) {
+        char* As = smem + buf * T::STAGE;
+        char* Bs = As + T::A_BYTES;
+#pragma unroll
+        for (int p = 0; p < T::A_PASSES; ++p) *reinterpret_cast<u32x4*>(As + swz(lr + 32 * p, lc)) = ra[p];
+#pragma unroll
+        for (int p = 0; p < T::B_PASSES; ++p) *reinterpret_cast<u32x4*>(Bs + swz(lr + 32 * p, lc)) = rb[p];
+    };
+
+    const int nk = a.K >> 6;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        if (kt + 1 < nk) gload((kt + 1) << 6);
+        const char* As = smem + (kt & 1) * T::STAGE;
+        const char* Bs = As + T::A_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int c = ks * 2 + (lane >> 5);
+            bf16x8 af[T::TM], bfr[T::TN];
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i)
+                af[i] = *reinterpret_cast<const bf16x8*>(As + swz(wm * T::WM + i * 32 + (lane & 31), c));
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j)
+                bfr[j] = *reinterpret_cast<const bf16x8*>(Bs + swz(wn * T::WN + j * 32 + (lane & 31), c));
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j) acc[i][j] = mfma32x32x16(af[i], bfr[j], acc[i][j]);
+        }
+        if (kt + 1 < nk) lstore((kt + 1) & 1);
+        __syncthreads();
+    }
+
+    // ---------------------------------------------------------------- epilogues
+    // acc[i][j][e] holds C[row][col] with
+    //   row = wm*WM + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = wn*WN + j*32 + lane%32.
+    const int lrow0 = wm * T::WM + 4 * (lane >> 5);
+    const int lcol0 = wn * T::WN + (lane & 31);
+
+    if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_F32_T) {
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int rl = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                if (rl >= rows) continue;
+                const int64_t orow = GROUPED ? (int64_t)row_base + rl : rl;
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j) {
+                    const int c = n0 + lcol0 + j * 32;
+                    if (c >= a.N) continue;
+                    const float v = acc[i][j][e];
+                    if constexpr (EPI == EPI_BF16)
+                        reinterpret_cast<bf16_t*>(a.out)[orow * a.ldo + c] = f32_to_bf16(v);
+                    else if constexpr (EPI == EPI_F32)
+                        reinterpret_cast<float*>(a.out)[orow * a.ldo + c] = v;
+                    else if constexpr (EPI == EPI_F32_T)
+                        reinterpret_cast<float*>(a.out)[(int64_t)c * a.ldo + orow] = v;
+                    else
+                        reinterpret_cast<float*>(a.out)[orow * a.ldo + c] += v;
+                }
+            }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        // Physical columns alternate 32 gate / 32 up; the pair (j, j+1) shares f.
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int rl = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                if (rl >= rows) continue;
+                const int64_t orow = GROUPED ? (int64_t)row_base + rl : rl;
+#pragma unroll
+                for (int j = 0; j < T::TN; j += 2) {
+                    const int c0 = n0 + wn * T::WN + j * 32;
+                    if (c0 >= a.N) continue;
+                    const int f = (c0 >> 1) + (lane & 31);
+                    const float gt = acc[i][j][e];
+                    const float up = acc[i][j + 1][e];
+                    const float h = gt / (1.f + __expf(-gt)) * up;
+                    reinterpret_cast<bf16_t*>(a.out)[orow * a.ldo + f] = f32_to_bf16(h);
+                }
+            }
+    } else if constexpr (EPI == EPI_QKV) {
+        if (a.head_dim == 128)
+            qkv_epilogue<T::TM, T::TN, 128>(a, acc, m0, rows, n0, lrow0, lcol0);
+        else
+            qkv_epilogue<T::TM, T::TN, 64>(a, acc, m0, rows, n0, lrow0, lcol0);
+    } else if constexpr (EPI == EPI_LMHEAD) {
+        // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
+        // sum exp(z - max)) over this tile's BM vocabulary rows.
+        SoftmaxPartial part[T::TN];
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j) {
+            float m = -INFINITY;
+            int idx = 0x7fffffff;
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                    const float z = (v < rows) ? acc[i][j][e] : -INFINITY;
+                    if (z > m) {
+                        m = z;
+                        idx = v;
+                    }
+                }
+            float s = 0.f;
+            if (m != -INFINITY) {
+                const float ml = m * kLog2e;
+#pragma unroll
+                for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                        if (v < rows) s += exp2f(acc[i][j][e] * kLog2e - ml);
+                    }
+            }
+            SoftmaxPartial p{m, idx, s};
+            SoftmaxPartial q;
+            q.m = __shfl_xor(p.m, 32, 64);
+            q.idx = __shfl_xor(p.idx, 32, 64);
+            q.s = __shfl_xor(p.s, 32, 64);
+            part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
+        }
+        // Merge the two waves that share these token columns (wm = 0, 1).
+        float4* xbuf = reinterpret_cast<float4*>(smem);
+        if (wm == 1 && lane < 32) {
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j)
+                xbuf[(wn * T::TN + j) * 32 + lane] =
+                    make_float4(part[j].m, __int_as_float(part[j].idx), part[j].s, 0.f);
+        }
+        __syncthreads();
+        if (wm == 0 && lane < 32) {
+            const int tile_m = m0 / BM;
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j) {
+                const int c = n0 + lcol0 + j * 32;
+                if (c >= a.N) continue;
+                const float4 o = xbuf[(wn * T::TN + j) * 32 + lane];
+                SoftmaxPartial other{o.x, __float_as_int(o.y), o.z};
+                SoftmaxPartial r = sp_merge(part[j], other);
+                a.partials[(int64_t)tile_m * a.N + c] = make_float4(r.m, __int_as_float(r.idx), r.s, 0.f);
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int EPI, bool GROUPED>
+hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
+    const int tiles_n = (a.N + BN - 1) / BN;
+    const int tiles_m = GROUPED ? max_tiles : (a.M + BM - 1) / BM;
+    int64_t blocks = (int64_t)tiles_m * tiles_n;
+    blocks = (blocks + 7) / 8 * 8;
+    if (blocks <= 0) return hipSuccess;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, EPI, GROUPED>), dim3((unsigned)blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int EPI, bool GROUPED>
+hipError_t launch_tiles(const GemmArgs& a, int bm, int bn, int max_tiles, hipStream_t st) {
+    if (bm == 256 && bn == 256) return launch_t<256, 256, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 256 && bn == 128) return launch_t<256, 128, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 128) return launch_t<128, 128, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 64) return launch_t<128, 64, EPI, GROUPED>(a, max_tiles, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmArgs& a, int epi, bool grouped, int bm, int bn, int max_tiles,
+                       hipStream_t st) {
+    if (a.K % 64 != 0 || a.N <= 0 || (!grouped && a.M <= 0)) return hipErrorInvalidValue;
+    switch (epi) {
+        case EPI_BF16:
+            return grouped ? launch_tiles<EPI_BF16, true>(a, bm, bn, max_tiles, st)
+                           : launch_tiles<EPI_BF16, false>(a, bm, bn, max_tiles, st);
+        case EPI_SWIGLU:
+            return grouped ? launch_tiles<EPI_SWIGLU, true>(a, bm, bn, max_tiles, st)
+                           : launch_tiles<EPI_SWIGLU, false>(a, bm, bn, max_tiles, st);
+        case EPI_F32:
+            return grouped ? hipErrorInvalidValue : launch_tiles<EPI_F32, false>(a, bm, bn, max_tiles, st);
+        case EPI_RESID:
+            return grouped ? hipErrorInvalidValue : launch_tiles<EPI_RESID, false>(a, bm, bn, max_tiles, st);
+        case EPI_QKV:
+            return grouped ? hipErrorInvalidValue : launch_tiles<EPI_QKV, false>(a, bm, bn, max_tiles, st);
+        case EPI_LMHEAD:
+            return grouped ? hipErrorInvalidValue : launch_tiles<EPI_LMHEAD, false>(a, bm, bn, max_tiles, st);
+        case EPI_F32_T:
+            return grouped ? hipErrorInvalidValue : launch_tiles<EPI_F32_T, false>(a, bm, bn, max_tiles, st);
+        default:
+            return hipErrorInvalidValue;
+    }
+}

@@ -1,0 +1,98 @@
+// Host-side launchers of the refinement-step kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;
+
+// ----------------------------------------------------------------- init.hip
+void launch_init_weights(bf16_t* dst, uint64_t n_phys, uint32_t cols, uint32_t tid_a,
+                         uint32_t tid_b, int layout, uint64_t seed, float c, hipStream_t st);
+void launch_fill_bf16(bf16_t* dst, uint64_t n, bf16_t v, hipStream_t st);
+void launch_rope_table(float2* tab, int S, int half, double theta, hipStream_t st);
+
+// ----------------------------------------------------------------- gemm.hip
+enum GemmEpilogue {
+    EPI_BF16 = 0,     // out_bf16[row][col]
+    EPI_F32 = 1,      // out_f32[row][col]
+    EPI_RESID = 2,    // resid_f32[row][col] += acc
+    EPI_SWIGLU = 3,   // out_bf16[row][f] = silu(gate) * up, gate/up interleaved in 32-col blocks
+    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K [B][KV][S][hd], Vt [B][KV][hd][S]
+    EPI_LMHEAD = 5,   // rows = vocab, cols = tokens: per-(vocab tile, token) softmax partials
+    EPI_F32_T = 6,    // out_f32[col][row] (transposed store)
+};
+
+struct GemmArgs {
+    // C[M x N] = A[M x K] * B[N x K]^T  (bf16 in, fp32 accumulate)
+    const bf16_t* A;
+    int64_t lda;
+    const bf16_t* B;
+    int64_t ldb;
+    int64_t b_group_stride;   // elements between consecutive groups' B (grouped mode)
+    int M, N, K;
+    // grouped mode (experts): tiles listed on the device
+    const int2* tile_tab;     // [max_tiles] (group, m0)
+    const int* n_tiles;       // device scalar: valid entries in tile_tab
+    const int* grp_off;       // [groups+1] row offsets (exclusive scan of group sizes)
+    const int* a_rows;        // optional gather: A row of permuted row r (NULL = identity)
+    int group_m;              // raster: m-tiles per raster group (dense mode)
+    // epilogue
+    void* out;
+    int64_t ldo;
+    // EPI_QKV
+    bf16_t* q;
+    bf16_t* k;
+    bf16_t* vt;
+    const float2* rope;       // [S][hd/2] (cos, sin)
+    int seq, seq_pad, n_heads, n_kv, head_dim;   // Vt rows are seq_pad long
+    // EPI_LMHEAD: partials [M/BM tiles][N] (m, idx, s) stored as float4
+    float4* partials;
+};
+
+// Launch one GEMM; bm/bn pick the tile (256x256, 256x128, 128x128, 128x64).
+// max_tiles (grouped mode): capacity of tile_tab.
+hipError_t launch_gemm(const GemmArgs& a, int epi, bool grouped, int bm, int bn, int max_tiles,
+                       hipStream_t st);
+
+// ----------------------------------------------------------------- attention.hip
+// Non-causal attention; O [B*S][H*hd] bf16.
+hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, bf16_t* o, int B,
+                            int S, int H, int KV, int hd, hipStream_t st);
+
+// ----------------------------------------------------------------- elementwise.hip
+void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
+                  hipStream_t st);
+void launch_rmsnorm(const float* x, const bf16_t* g, bf16_t* h, int rows, int d, float eps,
+                    hipStream_t st);
+// rows (b, P + i) for i < D of a [B][S] stream -> h [B*D][d]
+void launch_rmsnorm_draft_rows(const float* x, const bf16_t* g, bf16_t* h, int B, int S, int P,
+                               int D, int d, float eps, hipStream_t st);
+void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* top1, float* conf,
+                         float* max_logit, hipStream_t st);
+void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top1, const float* conf,
+                 float threshold, int mask_id, int32_t* counters, int32_t* out_top1,
+                 float* out_conf, hipStream_t st);
+void launch_apply_mask(const int32_t* prompt, const int32_t* draft, const uint8_t* mask,
+                       int32_t* tokens, int B, int P, int D, int mask_id, hipStream_t st);
+void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, int P, int D,
+                           hipStream_t st);
+void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int mask_id,
+                        int32_t* counter, hipStream_t st);
+void launch_zero_i32(int32_t* p, int n, hipStream_t st);
+
+// ----------------------------------------------------------------- moe.hip
+// Router softmax + top-k (ties -> lower id) + renormalisation; counts per expert.
+void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w,
+                 int32_t* counts, hipStream_t st);
+// Exclusive scan of counts (E routed + n_shared groups of T rows), tile table.
+void launch_dispatch_scan(int32_t* counts, int E, int n_shared, int T, int bm, int32_t* grp_off,
+                          int2* tile_tab, int32_t* n_tiles, int32_t* cursor, hipStream_t st);
+// Row permutation: slot[t][j] and a_rows[slot] = t.
+void launch_dispatch_scatter(const int32_t* ids, int T, int k, int E, int n_shared,
+                             const int32_t* grp_off, int32_t* cursor, int32_t* slot,
+                             int32_t* a_rows, hipStream_t st);
+// x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[shared rows]
+void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
+                    const int32_t* grp_off, int T, int k, int E, int n_shared, int d,
+                    hipStream_t st);

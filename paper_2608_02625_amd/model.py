@@ -1,0 +1,167 @@
+"""Python front end of the refinement-step library.
+
+PyTorch supplies device memory and the stream; every computation of the
+refinement pass runs in libdlm.so's HIP kernels through the C ABI.
+"""
+
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import DlmConfig, DlmStats, check
+
+CONFIG_FIELDS = [f for f, _ in DlmConfig._fields_]
+
+
+def make_config(shape) -> DlmConfig:
+    """DlmConfig from a mapping or an object with the dlm_config field names."""
+    get = (lambda k: shape[k]) if isinstance(shape, dict) else (lambda k: getattr(shape, k))
+    cfg = DlmConfig()
+    for f in CONFIG_FIELDS:
+        setattr(cfg, f, get(f))
+    return cfg
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+class Refiner:
+    """A refiner with synthetic weights resident in HBM.
+
+    shape: mapping/object with the dlm_config fields; seed: weight seed.
+    """
+
+    def __init__(self, shape, seed: int, device: str | torch.device = "cuda"):
+        self.lib = _lib.load()
+        self.device = torch.device(device)
+        self.cfg = make_config(shape)
+        nbytes = self.lib.dlm_weights_bytes(ctypes.byref(self.cfg))
+        if nbytes == 0:
+            raise ValueError("invalid refiner shape")
+        self.weights = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self._handle = ctypes.c_void_p()
+        check(self.lib.dlm_load_synthetic_weights(ctypes.byref(self.cfg), int(seed), self.weights.data_ptr(),
+                                                  nbytes, self.stream, ctypes.byref(self._handle)),
+              "dlm_load_synthetic_weights")
+        self._ws = {}
+
+    # -------------------------------------------------------------- plumbing
+    @property
+    def stream(self) -> int:
+        return torch.cuda.current_stream(self.device).cuda_stream
+
+    @property
+    def mask_id(self) -> int:
+        return int(self.cfg.mask_id)
+
+    def workspace(self, batch: int, prompt_len: int, draft_len: int) -> torch.Tensor:
+        key = (batch, prompt_len, draft_len)
+        ws = self._ws.get(key)
+        if ws is None:
+            n = self.lib.dlm_workspace_bytes(ctypes.byref(self.cfg), batch, prompt_len, draft_len)
+            if n == 0:
+                raise ValueError(f"invalid shape {key}")
+            ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+            self._ws[key] = ws
+        return ws
+
+    def close(self):
+        if getattr(self, "_handle", None) and self._handle.value:
+            self.lib.dlm_free(self._handle)
+            self._handle = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -------------------------------------------------------------- refinement
+    def refine_step(self, tokens: torch.Tensor, prompt_len: int, threshold: float,
+                    top1: torch.Tensor | None = None, conf: torch.Tensor | None = None,
+                    stats: torch.Tensor | None = None):
+        """One pass over tokens (int32 [B, S], updated in place)."""
+        B, S = tokens.shape
+        D = S - prompt_len
+        ws = self.workspace(B, prompt_len, D)
+        check(self.lib.dlm_refine_step(self._handle, B, prompt_len, D, tokens.data_ptr(), float(threshold),
+                                       ws.data_ptr(), ws.numel(), self.stream, _ptr(top1), _ptr(conf),
+                                       _ptr(stats)), "dlm_refine_step")
+        return tokens
+
+    def refine(self, prompt: torch.Tensor, draft: torch.Tensor, mask: torch.Tensor | None, n_steps: int,
+               threshold: float):
+        """Refine draft (int32 [B, D], in place) given prompt [B, P] and mask (uint8/bool [B, D])."""
+        B, P = prompt.shape
+        D = draft.shape[1]
+        ws = self.workspace(B, P, D)
+        m = None
+        if mask is not None:
+            m = mask.to(torch.uint8).contiguous()
+        st = DlmStats()
+        check(self.lib.dlm_refine(self._handle, B, P, D, prompt.data_ptr() if P else None, draft.data_ptr(),
+                                  _ptr(m), int(n_steps), float(threshold), ws.data_ptr(), ws.numel(), self.stream,
+                                  ctypes.byref(st)), "dlm_refine")
+        return draft, st.as_dict()
+
+    # -------------------------------------------------------------- test hooks
+    def debug_forward(self, tokens: torch.Tensor, prompt_len: int, want_logits: bool = False):
+        B, S = tokens.shape
+        D = S - prompt_len
+        ws = self.workspace(B, prompt_len, D)
+        dev = self.device
+        hidden = torch.empty(B * S, self.cfg.d_model, dtype=torch.float32, device=dev)
+        mx = torch.empty(B * D, dtype=torch.float32, device=dev)
+        t1 = torch.empty(B * D, dtype=torch.int32, device=dev)
+        cf = torch.empty(B * D, dtype=torch.float32, device=dev)
+        lg = torch.empty(B * D, self.cfg.vocab, dtype=torch.float32, device=dev) if want_logits else None
+        check(self.lib.dlm_debug_forward(self._handle, B, prompt_len, D, tokens.data_ptr(), ws.data_ptr(),
+                                         ws.numel(), self.stream, hidden.data_ptr(), mx.data_ptr(), t1.data_ptr(),
+                                         cf.data_ptr(), _ptr(lg)), "dlm_debug_forward")
+        out = {"hidden": hidden, "max_logit": mx, "top1": t1, "conf": cf}
+        if want_logits:
+            out["logits"] = lg
+        return out
+
+    def debug_layer(self, layer: int, x: torch.Tensor, batch: int, seq_len: int) -> torch.Tensor:
+        ws = self.workspace(batch, 0, seq_len)
+        y = torch.empty_like(x)
+        check(self.lib.dlm_debug_layer(self._handle, layer, batch, seq_len, x.data_ptr(), y.data_ptr(),
+                                       ws.data_ptr(), ws.numel(), self.stream), "dlm_debug_layer")
+        return y
+
+    def debug_head(self, x: torch.Tensor, batch: int, prompt_len: int, draft_len: int):
+        ws = self.workspace(batch, prompt_len, draft_len)
+        R = batch * draft_len
+        mx = torch.empty(R, dtype=torch.float32, device=self.device)
+        t1 = torch.empty(R, dtype=torch.int32, device=self.device)
+        cf = torch.empty(R, dtype=torch.float32, device=self.device)
+        check(self.lib.dlm_debug_head(self._handle, batch, prompt_len, draft_len, x.data_ptr(), ws.data_ptr(),
+                                      ws.numel(), self.stream, mx.data_ptr(), t1.data_ptr(), cf.data_ptr()),
+              "dlm_debug_head")
+        return {"max_logit": mx, "top1": t1, "conf": cf}
+
+    def weight_storage(self, layer_field: int, kind: int, expert: int = 0):
+        """(byte offset into self.weights, layout code) of one logical tensor."""
+        p = ctypes.c_void_p()
+        layout = ctypes.c_int32()
+        check(self.lib.dlm_weight_info(self._handle, layer_field, kind, expert, ctypes.byref(p),
+                                       ctypes.byref(layout)), "dlm_weight_info")
+        return p.value - self.weights.data_ptr(), layout.value
+
+    # -------------------------------------------------------------- profiling
+    def set_profiling(self, name_filter: str | None):
+        f = None if name_filter is None else name_filter.encode()
+        check(self.lib.dlm_set_profiling(self._handle, f), "dlm_set_profiling")
+
+    def profile_read(self, max_entries: int = 1 << 16):
+        names = (ctypes.c_char_p * max_entries)()
+        ms = (ctypes.c_float * max_entries)()
+        n = self.lib.dlm_profile_read(self._handle, names, ms, max_entries)
+        if n < 0:
+            raise _lib.DlmError("dlm_profile_read failed")
+        return [(names[i].decode(), float(ms[i])) for i in range(n)]

@@ -1,0 +1,87 @@
+"""CPU checks of the C ABI: the library loads, exports every declared entry point,
+and its host-side validation and size queries behave (no GPU work is launched)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dlm.h")
+
+
+def _lib():
+    from paper_2608_02625_amd import _lib as L
+    if not os.path.exists(L.LIB_PATH):
+        import paper_2608_02625_amd.build as b
+        b.build()
+    return L
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dlm_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ("dlm_load_synthetic_weights", "dlm_refine_step", "dlm_refine", "dlm_weights_bytes",
+              "dlm_workspace_bytes", "dlm_free", "dlm_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib()
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in _declared():
+        assert hasattr(lib, n), n
+    bound = {n for n, _, _ in L.SIGNATURES}
+    assert bound == set(_declared())
+
+
+def _cfg(L, **over):
+    from workloads import MODELS
+    from paper_2608_02625_amd.model import make_config
+    d = MODELS["mini_moe"].as_dict()
+    d.update(over)
+    return make_config(d)
+
+
+def test_size_queries_and_validation():
+    L = _lib()
+    lib = L.load()
+    cfg = _cfg(L)
+    wb = lib.dlm_weights_bytes(ctypes.byref(cfg))
+    # 20 layers of d 2048: QKV 3072x2048, O 2048x2048, router 64x2048, 65 experts of
+    # 3 x 1024x2048, plus embedding and LM head 157184x2048, all bf16 (+ gains, padding).
+    params = 20 * (3072 * 2048 + 2048 * 2048 + 64 * 2048 + 65 * 3 * 1024 * 2048) + 2 * 157184 * 2048
+    assert params * 2 <= wb <= params * 2 + 20 * 16 * 4096 + 4 * 4096 + 200 * 256 * 20
+    ws = lib.dlm_workspace_bytes(ctypes.byref(cfg), 8, 256, 384)
+    assert ws > 5120 * 2048 * 4
+    assert lib.dlm_workspace_bytes(ctypes.byref(cfg), 0, 256, 384) == 0
+    assert lib.dlm_workspace_bytes(ctypes.byref(cfg), 8, 256, 0) == 0
+    for bad in (dict(head_dim=96), dict(top_k=9), dict(mask_id=157184), dict(n_heads=15),
+                dict(expert_ffn_dim=100), dict(n_experts=300), dict(vocab=1)):
+        assert lib.dlm_weights_bytes(ctypes.byref(_cfg(L, **bad))) == 0, bad
+
+
+def test_errors_are_reported_without_gpu_work():
+    L = _lib()
+    lib = L.load()
+    h = ctypes.c_void_p()
+    bad = _cfg(L, head_dim=96)
+    st = lib.dlm_load_synthetic_weights(ctypes.byref(bad), 0, None, 0, None, ctypes.byref(h))
+    assert st == -1 and b"head_dim" in lib.dlm_last_error()
+    good = _cfg(L)
+    st = lib.dlm_load_synthetic_weights(ctypes.byref(good), 0, None, 0, None, ctypes.byref(h))
+    assert st == -1 and b"NULL" in lib.dlm_last_error()
+    st = lib.dlm_load_synthetic_weights(ctypes.byref(good), 0, ctypes.c_void_p(256), 1024, None, ctypes.byref(h))
+    assert st == -5 and b"too small" in lib.dlm_last_error()
+    assert lib.dlm_refine_step(None, 1, 1, 1, None, 0.5, None, 0, None, None, None, None) == -1
+    assert lib.dlm_refine(None, 1, 1, 1, None, None, None, 1, 0.5, None, 0, None, None) == -1
+    with pytest.raises(L.DlmError):
+        L.check(-1, "x")

@@ -1,0 +1,220 @@
+"""GPU parity of the HIP refinement step against the float64 CPU oracle.
+
+Same seeded synthetic weights and inputs on both sides.  Hidden states and
+logits must agree within max-abs-relative error 2e-2 (bf16 operands, fp32
+accumulation); top-1 tokens and edit decisions bit-exact wherever the oracle's
+top-1/top-2 logit margin and its distance from the threshold exceed 1e-2;
+final token sequences bit-exact on the tiny model.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from tests.gpu_util import HIDDEN_TOL, MARGIN, decisions_exempt, log, max_abs_rel, need_gpu
+from workloads import MODELS, WORKLOADS, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _cuda_i32(a):
+    torch = _torch()
+    return torch.tensor(np.ascontiguousarray(a, dtype=np.int32), device="cuda")
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def read_logical(R, layer_field, kind, expert, rows, cols):
+    """Logical [rows, cols] float32 view of one weight tensor in the GPU buffer."""
+    torch = _torch()
+    off, layout = R.weight_storage(layer_field, kind, expert)
+    n = rows * cols * (2 if layout == 1 else 1)
+    raw = _np(R.weights[off:off + 2 * n].view(torch.int16)).view(np.uint16)
+    if layout == 1:
+        phys = raw.reshape(rows // 32, 2, 32, cols)
+        part = 0 if kind in (4, 8, 11) else 1        # gate kinds take the first 32 rows of each block
+        raw = phys[:, part].reshape(rows, cols)
+    else:
+        raw = raw.reshape(rows, cols)
+    return (raw.astype(np.uint32) << 16).view(np.float32)
+
+
+def _setup(name, **over):
+    need_gpu()
+    import oracle
+    from paper_2608_02625_amd import Refiner
+    w = WORKLOADS[name]
+    shape = w.model.replace(**over) if over else w.model
+    log(f"[setup] {name} {over} building refiner on cuda:0")
+    R = Refiner(shape.as_dict(), w.weight_seed)
+    W = oracle.OracleWeights(shape, w.weight_seed)
+    return w, shape, R, W
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return _setup("tiny")
+
+
+def test_weights_bit_exact_tiny(tiny):
+    from oracle import weights as ow
+    w, s, R, W = tiny
+    d = s.d_model
+    assert np.array_equal(read_logical(R, 0, ow.K_EMBED, 0, s.vocab, d), W.embed())
+    assert np.array_equal(read_logical(R, 0, ow.K_LM_HEAD, 0, s.vocab, d), W.lm_head())
+    for l in range(s.n_layers):
+        L = W.layer(l)
+        f = l + 1
+        assert np.array_equal(read_logical(R, f, ow.K_WQ, 0, s.n_heads * s.head_dim, d), L["wq"])
+        assert np.array_equal(read_logical(R, f, ow.K_WK, 0, s.n_kv_heads * s.head_dim, d), L["wk"])
+        assert np.array_equal(read_logical(R, f, ow.K_WV, 0, s.n_kv_heads * s.head_dim, d), L["wv"])
+        assert np.array_equal(read_logical(R, f, ow.K_WO, 0, d, s.n_heads * s.head_dim), L["wo"])
+        assert np.array_equal(read_logical(R, f, ow.K_FFN_GATE, 0, s.ffn_dim, d), L["w_gate"])
+        assert np.array_equal(read_logical(R, f, ow.K_FFN_UP, 0, s.ffn_dim, d), L["w_up"])
+        assert np.array_equal(read_logical(R, f, ow.K_FFN_DOWN, 0, d, s.ffn_dim), L["w_down"])
+
+
+def _tokens(w, shape):
+    prompt, draft, mask = make_inputs(w)
+    return np.concatenate([prompt, np.where(mask, shape.mask_id, draft)], 1).astype(np.int32)
+
+
+def test_forward_tiny(tiny):
+    import oracle
+    w, s, R, W = tiny
+    toks = _tokens(w, s)
+    P, d = w.prompt_len, s.d_model
+    out = R.debug_forward(_cuda_i32(toks), P, want_logits=True)
+    x_ref = oracle.forward(W, toks)
+    red = oracle.lm_head_reduce(W, x_ref[:, P:].reshape(-1, d), want_logits=True)
+    eh = max_abs_rel(_np(out["hidden"]), x_ref.reshape(-1, d))
+    el = max_abs_rel(_np(out["logits"]), red["logits"])
+    em = max_abs_rel(_np(out["max_logit"]), red["max_logit"])
+    ec = max_abs_rel(_np(out["conf"]), red["conf"])
+    ok = red["margin"] > MARGIN
+    mism = int(np.sum((_np(out["top1"]) != red["top1"]) & ok))
+    log(f"[tiny forward] hidden {eh:.2e} logits {el:.2e} max_logit {em:.2e} conf {ec:.2e} "
+        f"top1 checked {int(ok.sum())}/{ok.size} mismatches {mism}")
+    assert eh <= HIDDEN_TOL and el <= HIDDEN_TOL and em <= HIDDEN_TOL and ec <= HIDDEN_TOL
+    assert mism == 0
+
+
+def test_refine_tiny_workload(tiny):
+    """The tiny workload itself (threshold 0.9, 4 steps, 30% masked): final tokens bit-exact."""
+    import oracle
+    torch = _torch()
+    w, s, R, W = tiny
+    prompt, draft, mask = make_inputs(w)
+    ref, st = oracle.refine(W, prompt, draft, mask, w.n_steps, w.threshold)
+    d_draft = _cuda_i32(draft)
+    _, gst = R.refine(_cuda_i32(prompt), d_draft, torch.tensor(mask, device="cuda"), w.n_steps, w.threshold)
+    log(f"[tiny refine] oracle {st['steps_run']} steps unmasked {st['n_unmasked']} edited {st['n_edited']}; "
+        f"gpu {gst}")
+    assert np.array_equal(_np(d_draft), ref)
+    assert gst["steps_run"] == st["steps_run"]
+    assert gst["n_unmasked"] == st["n_unmasked"] and gst["n_edited"] == st["n_edited"]
+    assert gst["n_masked_left"] == st["n_masked_left"]
+
+
+@pytest.fixture(scope="module")
+def tiny_sharp():
+    # Sharper LM head so that confidences span (0, 1) and the rule edits.
+    return _setup("tiny", lm_head_scale=30.0)
+
+
+def test_refine_tiny_sharp_teacher_forced(tiny_sharp):
+    import oracle
+    torch = _torch()
+    w, s, R, W = tiny_sharp
+    tau = 0.9
+    toks = _tokens(w, s)
+    P, D = w.prompt_len, w.draft_len
+    total_moves = 0
+    for step in range(w.n_steps):
+        ref_next, info = oracle.refine_step(W, toks, P, tau)
+        g = _cuda_i32(toks)
+        t1 = torch.empty(D, dtype=torch.int32, device="cuda")
+        cf = torch.empty(D, dtype=torch.float32, device="cuda")
+        stats = torch.zeros(4, dtype=torch.int32, device="cuda")
+        R.refine_step(g, P, tau, top1=t1, conf=cf, stats=stats)
+        got = _np(g)
+        ex = decisions_exempt(info["margin"], info["conf"], tau).reshape(1, D)
+        chk = ~ex
+        moved = int(np.sum(ref_next[:, P:] != toks[:, P:]))
+        total_moves += moved
+        log(f"[tiny sharp step {step}] moves {moved} checked {int(chk.sum())}/{D} "
+            f"unmasked {info['n_unmasked']} edited {info['n_edited']} gpu stats {_np(stats).tolist()}")
+        assert np.array_equal(got[:, :P], toks[:, :P])
+        assert np.array_equal(got[:, P:][chk], ref_next[:, P:][chk])
+        assert np.array_equal(_np(t1).reshape(1, D)[info["margin"].reshape(1, D) > MARGIN],
+                              info["top1"][info["margin"] > MARGIN])
+        assert max_abs_rel(_np(cf), info["conf"].reshape(-1)) <= HIDDEN_TOL
+        toks = ref_next
+    assert total_moves > 0
+
+
+def test_refine_tiny_sharp_final_sequence(tiny_sharp):
+    import oracle
+    torch = _torch()
+    w, s, R, W = tiny_sharp
+    prompt, draft, mask = make_inputs(w)
+    ref, st = oracle.refine(W, prompt, draft, mask, w.n_steps, 0.9)
+    d_draft = _cuda_i32(draft)
+    _, gst = R.refine(_cuda_i32(prompt), d_draft, torch.tensor(mask, device="cuda"), w.n_steps, 0.9)
+    log(f"[tiny sharp refine] oracle {st['steps_run']} steps unmasked {st['n_unmasked']} "
+        f"edited {st['n_edited']}; gpu {gst}")
+    assert st["n_unmasked"] + st["n_edited"] > 0
+    assert np.array_equal(_np(d_draft), ref)
+
+
+@pytest.fixture(scope="module")
+def small():
+    return _setup("small_moe")
+
+
+def test_weights_bit_exact_small_moe_sampled(small):
+    from oracle import weights as ow
+    w, s, R, W = small
+    d, F = s.d_model, s.expert_ffn_dim
+    L = W.layer(2)
+    assert np.array_equal(read_logical(R, 3, ow.K_ROUTER, 0, s.n_experts, d), L["w_router"])
+    for e in (0, 17, 31):
+        g, u, dn = L["experts"][e]
+        assert np.array_equal(read_logical(R, 3, ow.K_EXP_GATE, e, F, d), g)
+        assert np.array_equal(read_logical(R, 3, ow.K_EXP_UP, e, F, d), u)
+        assert np.array_equal(read_logical(R, 3, ow.K_EXP_DOWN, e, d, F), dn)
+    g, u, dn = L["shared"][0]
+    assert np.array_equal(read_logical(R, 3, ow.K_SH_GATE, 0, F, d), g)
+    assert np.array_equal(read_logical(R, 3, ow.K_SH_DOWN, 0, d, F), dn)
+
+
+def test_forward_small_moe(small):
+    import oracle
+    w, s, R, W = small
+    toks = _tokens(w, s)
+    P, d = w.prompt_len, s.d_model
+    out = R.debug_forward(_cuda_i32(toks), P)
+    x_ref, infos, _ = oracle.forward(W, toks, collect=True)
+    gap = np.min(np.stack([i["route_gap"] for i in infos]), axis=0).reshape(-1)   # [T]
+    keep = gap > MARGIN
+    hid = _np(out["hidden"])
+    ref = x_ref.reshape(-1, d)
+    eh = max_abs_rel(hid[keep], ref[keep])
+    eh_all = max_abs_rel(hid, ref)
+    red = oracle.lm_head_reduce(W, x_ref[:, P:].reshape(-1, d))
+    keep_d = keep.reshape(1, -1)[:, P:].reshape(-1) & (red["margin"] > MARGIN)
+    mism = int(np.sum((_np(out["top1"]) != red["top1"]) & keep_d))
+    em = max_abs_rel(_np(out["max_logit"])[keep_d], red["max_logit"][keep_d])
+    log(f"[small_moe forward] hidden {eh:.2e} (all tokens {eh_all:.2e}); route-exempt "
+        f"{int((~keep).sum())}/{keep.size}; max_logit {em:.2e}; top1 checked {int(keep_d.sum())} "
+        f"mismatches {mism}")
+    assert eh <= HIDDEN_TOL and em <= HIDDEN_TOL
+    assert mism == 0
