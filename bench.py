@@ -1,0 +1,206 @@
+"""Benchmark of the refinement step on one MI355X.
+
+A step is one refinement pass (non-causal forward over prompt+draft, fused
+top-1/confidence reduction over the vocabulary, threshold edit) over one batch
+of synthetic input resident in HBM.  Prints one JSON line with the throughput
+in refined (draft) positions per second, the roofline of the dominant kernel
+measured with HIP events inside the timed region, and the CPU oracle timed on
+a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15        # MI355X dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12         # MI355X HBM3E, B/s
+METRIC = "refined positions/sec per refinement step (1 GPU); MFMA % of bf16 peak"
+
+
+def step_flops(shape, B, P, D):
+    """Algorithmic FLOPs of one pass: active experts only, LM head on draft rows only."""
+    S = P + D
+    T = B * S
+    d, hd, H, KV = shape.d_model, shape.head_dim, shape.n_heads, shape.n_kv_heads
+    per_tok = d * (H + 2 * KV) * hd + H * hd * d
+    if shape.n_experts:
+        per_tok += d * shape.n_experts + (shape.top_k + shape.n_shared_experts) * 3 * d * shape.expert_ffn_dim
+    else:
+        per_tok += 3 * d * shape.ffn_dim
+    body = 2 * T * per_tok * shape.n_layers
+    attn = 4 * T * S * H * hd * shape.n_layers
+    head = 2 * B * D * d * shape.vocab
+    return body + attn + head
+
+
+def kernel_flops(name, shape, B, P, D):
+    """Algorithmic FLOPs of one launch of a named GEMM kernel."""
+    T = B * (P + D)
+    d = shape.d_model
+    if name == "gemm_expert_gate_up":
+        rows = T * (shape.top_k + shape.n_shared_experts)
+        return 2 * rows * d * 2 * shape.expert_ffn_dim
+    if name == "gemm_expert_down":
+        rows = T * (shape.top_k + shape.n_shared_experts)
+        return 2 * rows * shape.expert_ffn_dim * d
+    if name == "gemm_lm_head":
+        return 2 * B * D * d * shape.vocab
+    if name == "gemm_qkv":
+        return 2 * T * d * (shape.n_heads + 2 * shape.n_kv_heads) * shape.head_dim
+    if name == "gemm_o":
+        return 2 * T * shape.n_heads * shape.head_dim * d
+    if name == "attention":
+        return 4 * T * (P + D) * shape.n_heads * shape.head_dim
+    raise KeyError(name)
+
+
+def cpu_baseline(w, layers_sample=1):
+    """Oracle time for one batch row: `layers_sample` layers + the LM-head
+    reduction over that row's draft positions, extrapolated to all layers."""
+    import numpy as np
+    import oracle
+    from oracle.refine import layer_forward, lm_head_reduce
+    from workloads import make_inputs
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    shape = w.model
+    W = oracle.OracleWeights(shape, w.weight_seed, cache_layers=False)
+    prompt, draft, mask = make_inputs(w, batch=1)
+    tokens = np.concatenate([prompt, np.where(mask, shape.mask_id, draft)], 1).astype(np.int32)
+    x = W.embed_rows(tokens).astype(np.float64)
+    L = W.layer(0)
+    W.lm_head()
+    t0 = time.perf_counter()
+    for _ in range(layers_sample):
+        x, _ = layer_forward(shape, L, x)
+    t1 = time.perf_counter()
+    lm_head_reduce(W, x[0, w.prompt_len:])
+    t2 = time.perf_counter()
+    per_layer = (t1 - t0) / layers_sample
+    t_row = per_layer * shape.n_layers + (t2 - t1)
+    return {
+        "value": w.draft_len / t_row,
+        "unit": "refined positions/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"batch row 0 of {w.name} ({w.seq_len} tokens): {layers_sample} of {shape.n_layers} "
+                   f"layers timed ({per_layer:.2f} s/layer) + LM-head reduction over {w.draft_len} draft "
+                   f"positions ({t2 - t1:.2f} s), extrapolated to {shape.n_layers} layers; float64 NumPy; "
+                   f"weight generation not timed"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mini_moe")
+    ap.add_argument("--kernel", default="gemm_expert_gate_up", help="kernel reported in roofline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-table", action="store_true", help="also time every kernel (separate pass)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); multi-GPU sharding is not built",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_02625_amd import Refiner
+    from workloads import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    shape = w.model
+    B, P, D = w.batch, w.prompt_len, w.draft_len
+    torch.cuda.set_device(0)
+    print(f"[bench] workload {w.name}: B={B} P={P} D={D}; loading synthetic weights", file=sys.stderr, flush=True)
+    R = Refiner(shape.as_dict(), w.weight_seed)
+    prompt, draft, mask = make_inputs(w)
+    tokens0 = np.concatenate([prompt, np.where(mask, shape.mask_id, draft)], 1).astype(np.int32)
+    tokens = torch.tensor(tokens0, device="cuda")
+    R.workspace(B, P, D)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        R.refine_step(tokens, P, w.threshold)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
+
+    R.set_profiling(args.kernel)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        R.refine_step(tokens, P, w.threshold)
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    launches = R.profile_read()
+    R.set_profiling(None)
+    wall = t1 - t0
+    ms_step = wall * 1e3 / args.steps
+    ev_ms_step = ev0.elapsed_time(ev1) / args.steps
+
+    flops = step_flops(shape, B, P, D)
+    kt = [ms for (n, ms) in launches if n == args.kernel]
+    k_avg_ms = float(np.mean(kt)) if kt else float("nan")
+    k_flops = kernel_flops(args.kernel, shape, B, P, D)
+    achieved = k_flops / (k_avg_ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": B * D / (ms_step * 1e-3),
+        "unit": "refined positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "prompt_len": P, "draft_len": D,
+                   "n_layers": shape.n_layers, "d_model": shape.d_model, "n_experts": shape.n_experts,
+                   "top_k": shape.top_k, "vocab": shape.vocab, "threshold": w.threshold},
+        "step_mfma_frac": flops / (ms_step * 1e-3) / PEAK_BF16,
+        "step_tflops": flops / (ms_step * 1e-3) / 1e12,
+        "event_ms_per_step": ev_ms_step,
+        "roofline": {"kernel": args.kernel, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16 / 1e12,
+                     "unit": "TFLOP/s", "frac": achieved / (PEAK_BF16 / 1e12), "traffic": None,
+                     "launches": len(kt), "avg_ms": k_avg_ms, "flops_per_launch": k_flops},
+    }
+    if args.kernel_table:
+        R.set_profiling("*")
+        R.refine_step(tokens, P, w.threshold)
+        rows = R.profile_read()
+        R.set_profiling(None)
+        agg = {}
+        for n, ms in rows:
+            a = agg.setdefault(n, [0, 0.0])
+            a[0] += 1
+            a[1] += ms
+        out["kernel_table_ms"] = {n: round(v[1], 4) for n, v in sorted(agg.items(), key=lambda kv: -kv[1][1])}
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

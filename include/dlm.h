@@ -180,7 +180,7 @@ dlm_status dlm_weight_info(dlm_model* m, int32_t layer_field, int32_t kind, int3
 /*
  * Kernel timing with HIP events recorded on the launch stream around every
  * launch whose kernel name equals name_filter ("*" = every launch, NULL = off).
- * Recording restarts at each dlm_refine_step / dlm_refine call.
+ * Each dlm_set_profiling call clears what was recorded.
  * dlm_profile_read waits for the recorded events and writes up to max_entries
  * (kernel name, milliseconds) pairs, one per launch in launch order; it
  * returns the number written, or -1 on error.  Names are static strings.

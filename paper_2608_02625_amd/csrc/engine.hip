@@ -538,7 +538,6 @@ dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int3
     TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
     if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
     if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
-    m->prof_used = 0;
     Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
     return step_impl(x, d_tokens, threshold, d_top1, d_conf, d_stats);
 }
@@ -552,7 +551,6 @@ dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t d
     if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
     if (n_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_steps < 0");
     if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
-    m->prof_used = 0;
     Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
     int32_t* tokens = x.at<int32_t>(w.tokens);
     int32_t* counters = x.at<int32_t>(w.counters);

@@ -326,6 +326,7 @@ template <int EPI, bool GROUPED>
 hipError_t launch_tiles(const GemmArgs& a, int bm, int bn, int max_tiles, hipStream_t st) {
     if (bm == 256 && bn == 256) return launch_t<256, 256, EPI, GROUPED>(a, max_tiles, st);
     if (bm == 256 && bn == 128) return launch_t<256, 128, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 256) return launch_t<128, 256, EPI, GROUPED>(a, max_tiles, st);
     if (bm == 128 && bn == 128) return launch_t<128, 128, EPI, GROUPED>(a, max_tiles, st);
     if (bm == 128 && bn == 64) return launch_t<128, 64, EPI, GROUPED>(a, max_tiles, st);
     return hipErrorInvalidValue;

@@ -50,7 +50,7 @@ struct GemmArgs {
     float4* partials;
 };
 
-// Launch one GEMM; bm/bn pick the tile (256x256, 256x128, 128x128, 128x64).
+// Launch one GEMM; bm/bn pick the tile (256x256, 256x128, 128x256, 128x128, 128x64).
 // max_tiles (grouped mode): capacity of tile_tab.
 hipError_t launch_gemm(const GemmArgs& a, int epi, bool grouped, int bm, int bn, int max_tiles,
                        hipStream_t st);
