@@ -170,6 +170,13 @@ dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32
                           const float* d_x, void* d_workspace, size_t workspace_bytes,
                           void* hip_stream, float* d_max_logit, int32_t* d_top1, float* d_conf);
 
+/* dlm_debug_gemm: the library's bf16 MFMA GEMM on its own (for tests and
+ *   measurements): d_c float [m][n] = d_a bf16 [m][k] * d_b bf16 [n][k]^T, with a
+ *   tile of tile_m x tile_n (256x256, 256x128, 128x256, 128x128 or 128x64);
+ *   k must be a multiple of 64. */
+dlm_status dlm_debug_gemm(const void* d_a, const void* d_b, float* d_c, int32_t m, int32_t n,
+                          int32_t k, int32_t tile_m, int32_t tile_n, void* hip_stream);
+
 /* Device pointer and byte size of one logical weight tensor (for tests):
  * kind/layer/expert as in dlm_load_synthetic_weights; *d_ptr receives the
  * base of the tensor's storage and *layout a code: 0 = plain row-major

@@ -52,6 +52,7 @@ SIGNATURES = [
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
     ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),
+    ("dlm_debug_gemm", _I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),
     ("dlm_weight_info", _I, [_P, _I, _I, _I, ctypes.POINTER(_P), ctypes.POINTER(_I)]),
     ("dlm_set_profiling", _I, [_P, ctypes.c_char_p]),
     ("dlm_profile_read", _I, [_P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_F), _I]),

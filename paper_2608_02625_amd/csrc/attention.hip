@@ -11,7 +11,8 @@
 // S^T = K Q^T, so that each lane owns one query column: the online-softmax
 // statistics stay lane-local (plus one exchange with lane^32), and the
 // probabilities feed the next MFMA directly from registers as the B operand of
-// O^T = V^T P^T, with the matching key order read from the V^T tile.
+// O^T = V^T P^T, with the matching key order read from the V^T tile.  V is
+// stored row-major like K and transposed while it is written to LDS.
 #include "common.h"
 #include "kernels.h"
 
@@ -27,7 +28,7 @@ struct AttnCfg {
     static constexpr int STAGE = K_BYTES + V_BYTES;
     static constexpr int K_CHUNKS_ROW = HD / 8;       // 16-byte chunks per K row
     static constexpr int K_PASSES = KEYS * K_CHUNKS_ROW / 256;
-    static constexpr int V_PASSES = HD * 8 / 256;     // V^T rows have 8 chunks
+    static constexpr int V_PASSES = HD / 8 / 4;       // 16-byte V chunks per lane (lane = key)
     static constexpr int NB = HD / 32;                // 32-row blocks of O^T
     static constexpr int NKS = HD / 16;               // K16 steps over hd
 };
@@ -35,8 +36,8 @@ struct AttnCfg {
 template <int HD>
 __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
                                                    const bf16_t* __restrict__ K,
-                                                   const bf16_t* __restrict__ Vt,
-                                                   bf16_t* __restrict__ O, int S, int S_pad, int H,
+                                                   const bf16_t* __restrict__ V,
+                                                   bf16_t* __restrict__ O, int S, int H,
                                                    int KV, float scale_log2) {
     using C = AttnCfg<HD>;
     __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
@@ -49,7 +50,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
 
     const bf16_t* Qh = Q + ((int64_t)b * H + h) * S * HD;
     const bf16_t* Kh = K + ((int64_t)b * KV + kvh) * S * HD;
-    const bf16_t* Vh = Vt + ((int64_t)b * KV + kvh) * HD * S_pad;
+    const bf16_t* Vh = V + ((int64_t)b * KV + kvh) * S * HD;
 
     bf16x8 qf[C::NKS];
     {
@@ -69,7 +70,6 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
     u32x4 rk[C::K_PASSES], rv[C::V_PASSES];
     const int kc = tid % C::K_CHUNKS_ROW, kr = tid / C::K_CHUNKS_ROW;
     constexpr int K_ROWS_PER_PASS = 256 / C::K_CHUNKS_ROW;
-    const int vc = tid & 7, vr = tid >> 3;
 
     auto gload = [&](int k0) {
 #pragma unroll
@@ -81,18 +81,10 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
         }
 #pragma unroll
         for (int p = 0; p < C::V_PASSES; ++p) {
-            const int row = vr + p * 32;
-            const int key = k0 + vc * 8;
-            u32x4 v = *reinterpret_cast<const u32x4*>(Vh + (int64_t)row * S_pad + key);
-            if (key + 8 > S) {
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    uint32_t m = 0u;
-                    if (key + 2 * w < S) m |= 0xffffu;
-                    if (key + 2 * w + 1 < S) m |= 0xffff0000u;
-                    v[w] &= m;
-                }
-            }
+            const int key = k0 + lane;
+            const int chunk = wave + 4 * p;
+            u32x4 v = *reinterpret_cast<const u32x4*>(Vh + (int64_t)min(key, S - 1) * HD + chunk * 8);
+            if (key >= S) v = u32x4{0u, 0u, 0u, 0u};
             rv[p] = v;
         }
     };
@@ -104,9 +96,10 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
             *reinterpret_cast<u32x4*>(Ks + (kr + p * K_ROWS_PER_PASS) * C::K_STRIDE + kc * 16) = rk[p];
 #pragma unroll
         for (int p = 0; p < C::V_PASSES; ++p) {
-            char* dst = Vs + (vr + p * 32) * C::V_STRIDE + vc * 16;
-            *reinterpret_cast<u32x2*>(dst) = u32x2{rv[p][0], rv[p][1]};
-            *reinterpret_cast<u32x2*>(dst + 8) = u32x2{rv[p][2], rv[p][3]};
+            char* dst = Vs + (wave + 4 * p) * 8 * C::V_STRIDE + lane * 2;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                *reinterpret_cast<bf16_t*>(dst + i * C::V_STRIDE) = (bf16_t)(rv[p][i >> 1] >> (16 * (i & 1)));
         }
     };
 
@@ -202,15 +195,14 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
 
 }  // namespace
 
-hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, bf16_t* o, int B,
+hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* v, bf16_t* o, int B,
                             int S, int H, int KV, int hd, hipStream_t st) {
-    const int S_pad = (S + 63) / 64 * 64;
     const dim3 grid((S + 127) / 128, H, B);
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     if (hd == 128)
-        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, S, S_pad, H, KV, scale_log2);
+        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, v, o, S, H, KV, scale_log2);
     else if (hd == 64)
-        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, S, S_pad, H, KV, scale_log2);
+        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, v, o, S, H, KV, scale_log2);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

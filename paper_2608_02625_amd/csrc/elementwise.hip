@@ -5,8 +5,6 @@
 
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
-
 // x[t][:] = E[tok[t]][:] (bf16 -> fp32); one workgroup per token.
 // Ids outside [0, V) are clamped into range so that no read leaves the table.
 __global__ void embed_kernel(const int32_t* __restrict__ tok, const bf16_t* __restrict__ emb,
@@ -80,31 +78,36 @@ __global__ void rmsnorm_draft_kernel(const float* __restrict__ x, const bf16_t* 
     rmsnorm_row(x + ((int64_t)b * S + P + i) * d, g, h + (int64_t)r * d, d, eps);
 }
 
-// Merge per-vocabulary-tile partials in tile order (deterministic).
-__global__ void lmhead_merge_kernel(const float4* __restrict__ part, int n_tiles, int R,
-                                    int32_t* __restrict__ top1, float* __restrict__ conf,
-                                    float* __restrict__ max_logit) {
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= R) return;
-    float m = -INFINITY;
-    int idx = 0x7fffffff;
-    for (int t = 0; t < n_tiles; ++t) {
-        const float4 p = part[(int64_t)t * R + r];
-        const int pi = __float_as_int(p.y);
-        if (p.x > m || (p.x == m && pi < idx)) {
-            m = p.x;
-            idx = pi;
+// Merge the per-vocabulary-tile partials of each row.  A workgroup handles 32
+// rows; each of the 8 thread groups of a row takes every 8th
+// tile (online merge in tile order), then the 8 group results are merged in
+// group order through LDS.  The order is fixed, so results are deterministic;
+// ties keep the lower vocabulary id.
+__global__ __launch_bounds__(256) void lmhead_merge_kernel(const float4* __restrict__ part, int n_tiles, int R,
+                                                           int32_t* __restrict__ top1, float* __restrict__ conf,
+                                                           float* __restrict__ max_logit) {
+    __shared__ float4 red[8][32];
+    const int rl = threadIdx.x & 31, split = threadIdx.x >> 5;
+    const int r = blockIdx.x * 32 + rl;
+    SoftmaxPartial acc{-INFINITY, 0x7fffffff, 0.f};
+    if (r < R) {
+        for (int t = split; t < n_tiles; t += 8) {
+            const float4 p = part[(int64_t)t * R + r];
+            acc = sp_merge(acc, SoftmaxPartial{p.x, __float_as_int(p.y), p.z});
         }
     }
-    float s = 0.f;
-    const float ml = m * kLog2e;
-    for (int t = 0; t < n_tiles; ++t) {
-        const float4 p = part[(int64_t)t * R + r];
-        if (p.z != 0.f) s += p.z * exp2f(p.x * kLog2e - ml);
+    red[split][rl] = make_float4(acc.m, __int_as_float(acc.idx), acc.s, 0.f);
+    __syncthreads();
+    if (split == 0 && r < R) {
+        SoftmaxPartial a = acc;
+        for (int q = 1; q < 8; ++q) {
+            const float4 p = red[q][rl];
+            a = sp_merge(a, SoftmaxPartial{p.x, __float_as_int(p.y), p.z});
+        }
+        top1[r] = a.idx;
+        conf[r] = 1.f / a.s;
+        if (max_logit) max_logit[r] = a.m;
     }
-    top1[r] = idx;
-    conf[r] = 1.f / s;
-    if (max_logit) max_logit[r] = m;
 }
 
 // Threshold rule, all draft slots at once from the same forward pass.
@@ -195,7 +198,7 @@ void launch_rmsnorm_draft_rows(const float* x, const bf16_t* g, bf16_t* h, int B
 
 void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* top1, float* conf,
                          float* max_logit, hipStream_t st) {
-    hipLaunchKernelGGL(lmhead_merge_kernel, dim3((R + 255) / 256), dim3(256), 0, st, partials,
+    hipLaunchKernelGGL(lmhead_merge_kernel, dim3((R + 31) / 32), dim3(256), 0, st, partials,
                        n_tiles, R, top1, conf, max_logit);
 }
 

@@ -161,7 +161,7 @@ WeightPlan plan_weights(const dlm_config& c) {
 // Workspace carve-up for one (B, P, D).
 struct Workspace {
     size_t total = 0;
-    size_t x, h, q, k, vt, attn, rope, hf, logits, ids, wts, counts, cursor, grp_off, tile_tab,
+    size_t x, h, q, k, v, attn, rope, hf, logits, ids, wts, grp_off, tile_tab,
         n_tiles, slot, a_rows, hexp, y, hfin, partials, top1, conf, maxlogit, counters, tokens;
     int rows_total = 0, max_tiles = 0, n_vtiles = 0;
 };
@@ -172,7 +172,6 @@ constexpr int kHeadBM = 256, kHeadBN = 256;
 Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
     Workspace w;
     const int64_t S = P + D, T = (int64_t)B * S, R = (int64_t)B * D;
-    const int64_t S_pad = (S + 63) / 64 * 64;
     const int d = c.d_model, hd = c.head_dim;
     auto add = [&](int64_t bytes) {
         const size_t off = w.total;
@@ -183,7 +182,7 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
     w.h = add(T * d * 2);
     w.q = add((int64_t)B * c.n_heads * S * hd * 2);
     w.k = add((int64_t)B * c.n_kv_heads * S * hd * 2);
-    w.vt = add((int64_t)B * c.n_kv_heads * hd * S_pad * 2);
+    w.v = add((int64_t)B * c.n_kv_heads * S * hd * 2);
     w.attn = add(T * c.n_heads * hd * 2);
     w.rope = add(S * (hd / 2) * 8);
     if (c.n_experts == 0) {
@@ -195,8 +194,6 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
         w.logits = add(T * E * 4);
         w.ids = add(T * k * 4);
         w.wts = add(T * k * 4);
-        w.counts = add(E * 4);
-        w.cursor = add(G * 4);
         w.grp_off = add((G + 1) * 4);
         w.tile_tab = add((int64_t)w.max_tiles * 8);
         w.n_tiles = add(4);
@@ -328,7 +325,7 @@ dlm_status run_layer(Ctx& x, int l) {
     bf16_t* h = x.at<bf16_t>(x.w.h);
     bf16_t* q = x.at<bf16_t>(x.w.q);
     bf16_t* k = x.at<bf16_t>(x.w.k);
-    bf16_t* vt = x.at<bf16_t>(x.w.vt);
+    bf16_t* v = x.at<bf16_t>(x.w.v);
     bf16_t* attn = x.at<bf16_t>(x.w.attn);
 
     LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g1), h, x.T, d, c.norm_eps, x.st));
@@ -337,10 +334,9 @@ dlm_status run_layer(Ctx& x, int l) {
         GemmArgs a = gemm_args(h, d, x.wt(L.wqkv), d, x.T, N, d);
         a.q = q;
         a.k = k;
-        a.vt = vt;
+        a.v = v;
         a.rope = x.at<float2>(x.w.rope);
         a.seq = x.S;
-        a.seq_pad = (x.S + 63) / 64 * 64;
         a.n_heads = H;
         a.n_kv = KV;
         a.head_dim = hd;
@@ -348,7 +344,7 @@ dlm_status run_layer(Ctx& x, int l) {
     }
     {
         prof_begin(x, "attention");
-        hipError_t e = launch_attention(q, k, vt, attn, x.B, x.S, H, KV, hd, x.st);
+        hipError_t e = launch_attention(q, k, v, attn, x.B, x.S, H, KV, hd, x.st);
         prof_end(x, "attention");
         if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("attention: ") + hipGetErrorString(e));
     }
@@ -376,8 +372,6 @@ dlm_status run_layer(Ctx& x, int l) {
     float* logits = x.at<float>(x.w.logits);
     int32_t* ids = x.at<int32_t>(x.w.ids);
     float* wts = x.at<float>(x.w.wts);
-    int32_t* counts = x.at<int32_t>(x.w.counts);
-    int32_t* cursor = x.at<int32_t>(x.w.cursor);
     int32_t* grp_off = x.at<int32_t>(x.w.grp_off);
     int2* tile_tab = x.at<int2>(x.w.tile_tab);
     int32_t* n_tiles = x.at<int32_t>(x.w.n_tiles);
@@ -391,11 +385,9 @@ dlm_status run_layer(Ctx& x, int l) {
         a.ldo = E;
         TRY(gemm(x, "gemm_router", a, EPI_F32, false, 128, 64, 0));
     }
-    LAUNCH(x, "topk", launch_topk(logits, x.T, E, kk, ids, wts, counts, x.st));
-    LAUNCH(x, "dispatch_scan",
-           launch_dispatch_scan(counts, E, NS, x.T, kExpertBM, grp_off, tile_tab, n_tiles, cursor, x.st));
-    LAUNCH(x, "dispatch_scatter",
-           launch_dispatch_scatter(ids, x.T, kk, E, NS, grp_off, cursor, slot, a_rows, x.st));
+    LAUNCH(x, "topk", launch_topk(logits, x.T, E, kk, ids, wts, x.st));
+    LAUNCH(x, "dispatch", launch_dispatch(ids, x.T, kk, E, NS, kExpertBM, grp_off, tile_tab, n_tiles, slot,
+                                          a_rows, x.st));
     {
         GemmArgs a = gemm_args(h, d, x.wt(L.wgu), d, 0, 2 * F, d);
         a.b_group_stride = (int64_t)2 * F * d;
@@ -425,7 +417,6 @@ dlm_status run_layer(Ctx& x, int l) {
 dlm_status run_prologue(Ctx& x, const int32_t* tokens) {
     const dlm_config& c = x.c;
     LAUNCH(x, "rope_table", launch_rope_table(x.at<float2>(x.w.rope), x.S, c.head_dim / 2, (double)c.rope_theta, x.st));
-    if (c.n_experts > 0) LAUNCH(x, "zero", launch_zero_i32(x.at<int32_t>(x.w.counts), c.n_experts, x.st));
     if (tokens) LAUNCH(x, "embed", launch_embed(tokens, x.wt(x.m->plan.emb), x.at<float>(x.w.x), x.T, c.d_model, c.vocab, x.st));
     return DLM_OK;
 }
@@ -630,6 +621,18 @@ dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32
     if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
     if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
     if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
+    return DLM_OK;
+}
+
+dlm_status dlm_debug_gemm(const void* d_a, const void* d_b, float* d_c, int32_t m, int32_t n, int32_t k,
+                          int32_t tile_m, int32_t tile_n, void* hip_stream) {
+    if (!d_a || !d_b || !d_c) return fail(DLM_ERR_INVALID_ARG, "NULL argument");
+    if (m <= 0 || n <= 0 || k <= 0 || k % 64) return fail(DLM_ERR_INVALID_ARG, "bad GEMM shape");
+    GemmArgs a = gemm_args((const bf16_t*)d_a, k, (const bf16_t*)d_b, k, m, n, k);
+    a.out = d_c;
+    a.ldo = n;
+    hipError_t e = launch_gemm(a, EPI_F32, false, tile_m, tile_n, 0, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return fail(DLM_ERR_INVALID_ARG, std::string("gemm: ") + hipGetErrorString(e));
     return DLM_OK;
 }
 

@@ -3,8 +3,9 @@
 // C[M x N] = A[M x K] * B[N x K]^T, fp32 accumulation, both operands K-contiguous.
 // A workgroup of 256 threads (4 waves in a 2x2 grid) owns a BM x BN tile; each
 // wave owns (BM/2) x (BN/2) as a grid of 32x32 accumulators fed by
-// v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through two LDS stages
-// (register-staged global loads for stage k+1 overlap the MFMAs of stage k).
+// v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through two LDS stages:
+// the global->LDS loads of stage k+1 (direct to LDS, no register staging) are
+// in flight while the MFMAs of stage k run.
 // LDS rows are 128 bytes (64 bf16) with 16-byte chunks XOR-swizzled by row
 // bits so that fragment reads of 32 consecutive rows spread over all banks.
 //
@@ -29,62 +30,87 @@ struct TileCfg {
     static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
     static constexpr int STAGE = A_BYTES + B_BYTES;
     static constexpr int LDS = 2 * STAGE;
-    static constexpr int A_PASSES = BM / 32, B_PASSES = BN / 32;
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) {
-    return row * 128 + ((chunk ^ ((row & 7) ^ ((row >> 3) & 1))) << 4);
-}
+__device__ __forceinline__ int swz_key(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+// Byte offset of logical 16-byte chunk `chunk` of tile row `row` (128-byte rows).
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ swz_key(row)) << 4); }
 
 // QKV projection epilogue: RoPE (rotate-half) on the q and k columns, then
-// scatter to Q [B][H][S][hd], K [B][KV][S][hd] and V^T [B][KV][hd][seq_pad].
-// A wave's column range covers whole heads, so the rotation partners
-// (i, i + hd/2) sit in the same lane, subtiles j and j + hd/64.
-template <int TM, int TN, int HD>
-__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0,
-                                             int rows, int n0, int lrow0, int lcol0) {
+// Q [B][H][S][hd], K and V [B][KV][S][hd] stored row-major.  A wave's column
+// range covers whole heads, so the rotation partners (i, i + hd/2) sit in the
+// same lane, subtiles j and j + hd/64.  The rotated tile is staged in LDS as
+// bf16 so that the stores are 16-byte row chunks.
+template <int BM, int BN, int HD>
+struct QkvEpi {
+    static constexpr int CS = BN * 2 + 16;       // LDS row stride (bytes)
+    static constexpr int LDS = BM * CS;
+};
+
+template <int BM, int BN, int TM, int TN, int HD>
+__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int rows,
+                                             int n0, int lrow0, int lcol0, char* smem) {
     constexpr int HALF = HD / 2, SPT = HD / 32, POFF = HD / 64;
+    constexpr int CS = QkvEpi<BM, BN, HD>::CS;
     const int Hq = a.n_heads * HD, Hk = a.n_kv * HD;
     const int S = a.seq;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            const int row = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-            if (row >= rows) continue;
-            const int b = row / S, s = row - b * S;
+            const int rl = lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+            const int row = m0 + rl;
+            const int s = (row < rows) ? row % S : 0;
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int c = n0 + lcol0 + j * 32;
-                if (c >= a.N) continue;
+                const int cl = lcol0 + j * 32;
+                const int c = n0 + cl;
+                float v = acc[i][j][e];
                 if (c < Hq + Hk) {
-                    if ((j % SPT) < POFF && j + POFF < TN) {
-                        const int hi = c % HD;            // < HALF
-                        const float2 cs = a.rope[s * HALF + hi];
-                        const float x1 = acc[i][j][e], x2 = acc[i][(j + POFF) % TN][e];
-                        const float o1 = x1 * cs.x - x2 * cs.y;
-                        const float o2 = x2 * cs.x + x1 * cs.y;
-                        bf16_t* dst;
-                        if (c < Hq)
-                            dst = a.q + (((int64_t)b * a.n_heads + c / HD) * S + s) * HD;
-                        else
-                            dst = a.k + (((int64_t)b * a.n_kv + (c - Hq) / HD) * S + s) * HD;
-                        dst[hi] = f32_to_bf16(o1);
-                        dst[hi + HALF] = f32_to_bf16(o2);
+                    if ((j % SPT) < POFF) {
+                        const float2 cs = a.rope[s * HALF + (c % HD)];
+                        v = v * cs.x - acc[i][(j + POFF) % TN][e] * cs.y;
+                    } else {
+                        const float2 cs = a.rope[s * HALF + (c % HD) - HALF];
+                        v = v * cs.x + acc[i][(j + TN - POFF) % TN][e] * cs.y;
                     }
-                } else {
-                    const int cv = c - Hq - Hk;
-                    const int kh = cv / HD, hi = cv - kh * HD;
-                    a.vt[(((int64_t)b * a.n_kv + kh) * HD + hi) * a.seq_pad + s] = f32_to_bf16(acc[i][j][e]);
                 }
+                *reinterpret_cast<bf16_t*>(smem + rl * CS + cl * 2) = f32_to_bf16(v);
             }
         }
+    __syncthreads();
+    constexpr int CPR = BN / 8;                  // 16-byte chunks per row
+    for (int q = threadIdx.x; q < BM * CPR; q += 256) {
+        const int rl = q / CPR, ch = q - rl * CPR;
+        const int row = m0 + rl;
+        const int c = n0 + ch * 8;
+        if (row >= rows || c >= a.N) continue;
+        const int b = row / S, s = row - b * S;
+        bf16_t* dst;
+        if (c < Hq) {
+            dst = a.q + (((int64_t)b * a.n_heads + c / HD) * S + s) * HD + (c % HD);
+        } else if (c < Hq + Hk) {
+            const int ck = c - Hq;
+            dst = a.k + (((int64_t)b * a.n_kv + ck / HD) * S + s) * HD + (ck % HD);
+        } else {
+            const int cv = c - Hq - Hk;
+            dst = a.v + (((int64_t)b * a.n_kv + cv / HD) * S + s) * HD + (cv % HD);
+        }
+        *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(smem + rl * CS + ch * 16);
+    }
+}
+
+template <int BM, int BN, int EPI>
+constexpr int epi_lds() {
+    return EPI == EPI_QKV ? QkvEpi<BM, BN, 128>::LDS : 0;
 }
 
 template <int BM, int BN, int EPI, bool GROUPED>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     using T = TileCfg<BM, BN>;
-    __shared__ __attribute__((aligned(16))) char smem[T::LDS];
+    constexpr int LDS_BYTES = T::LDS > epi_lds<BM, BN, EPI>() ? T::LDS : epi_lds<BM, BN, EPI>();
+    __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -128,23 +154,41 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     const bf16_t* Bg = a.B + (GROUPED ? (int64_t)g * a.b_group_stride : 0);
 
     // ---------------------------------------------------------------- main loop
-    const int lc = tid & 7, lr = tid >> 3;
-    const bf16_t* a_ptr[T::A_PASSES];
-    const bf16_t* b_ptr[T::B_PASSES];
+    // Operands go global -> LDS directly (global_load_lds_dwordx4): one
+    // instruction per wave fills a contiguous 1 KB block = 8 tile rows of 128 B,
+    // lane L writing bytes [16L, 16L+16).  The XOR swizzle of the 16-byte
+    // chunks is applied on the global side: the lane that fills physical chunk
+    // pc of row r fetches logical chunk pc ^ f(r).
+    constexpr int A_INSTR = BM / 32, B_INSTR = BN / 32;        // 1 KB blocks per wave
+    const int wv = uniform(wave);
+    const int rin = lane >> 3, pc = lane & 7;
+    const bf16_t* a_src[A_INSTR];
+    const bf16_t* b_src[B_INSTR];
 #pragma unroll
-    for (int p = 0; p < T::A_PASSES; ++p) {
-        const int r = min(m0 + lr + 32 * p, rows - 1);
+    for (int p = 0; p < A_INSTR; ++p) {
+        const int tr = (wv * A_INSTR + p) * 8 + rin;               // row within the tile
+        const int r = min(m0 + tr, rows - 1);
         int64_t grow = r;
         if (GROUPED) grow = a.a_rows ? a.a_rows[row_base + r] : row_base + r;
-        a_ptr[p] = a.A + grow * a.lda + lc * 8;
+        a_src[p] = a.A + grow * a.lda + (pc ^ swz_key(tr)) * 8;
     }
 #pragma unroll
-    for (int p = 0; p < T::B_PASSES; ++p) {
-        const int n = min(n0 + lr + 32 * p, a.N - 1);
-        b_ptr[p] = Bg + (int64_t)n * a.ldb + lc * 8;
+    for (int p = 0; p < B_INSTR; ++p) {
+        const int tr = (wv * B_INSTR + p) * 8 + rin;
+        const int n = min(n0 + tr, a.N - 1);
+        b_src[p] = Bg + (int64_t)n * a.ldb + (pc ^ swz_key(tr)) * 8;
     }
+    auto issue = [&](int k0, int stage) {
+        char* As = smem + stage * T::STAGE;
+        char* Bs = As + T::A_BYTES;
+#pragma unroll
+        for (int p = 0; p < A_INSTR; ++p)
+            lds_dma16(a_src[p] + k0, As + (wv * A_INSTR + p) * 1024);
+#pragma unroll
+        for (int p = 0; p < B_INSTR; ++p)
+            lds_dma16(b_src[p] + k0, Bs + (wv * B_INSTR + p) * 1024);
+    };
 
-    u32x4 ra[T::A_PASSES], rb[T::B_PASSES];
     f32x16 acc[T::TM][T::TN];
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
@@ -153,47 +197,64 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int p = 0; p < T::A_PASSES; ++p) ra[p] = *reinterpret_cast<const u32x4*>(a_ptr[p] + k0);
-#pragma unroll
-        for (int p = 0; p < T::B_PASSES; ++p) rb[p] = *reinterpret_cast<const u32x4*>(b_ptr[p] + k0);
-    };
-    auto lstore = [&](int buf) {
-        char* As = smem + buf * T::STAGE;
-        char* Bs = As + T::A_BYTES;
-#pragma unroll
-        for (int p = 0; p < T::A_PASSES; ++p) *reinterpret_cast<u32x4*>(As + swz(lr + 32 * p, lc)) = ra[p];
-#pragma unroll
-        for (int p = 0; p < T::B_PASSES; ++p) *reinterpret_cast<u32x4*>(Bs + swz(lr + 32 * p, lc)) = rb[p];
-    };
-
+    // Software pipeline (per 64-wide K tile kt, LDS stage kt&1):
+    //   registers R hold all fragments of tile kt; the MFMAs of step ks run
+    //   while the fragments of tile kt+1 step ks-1 are read into the slot that
+    //   step ks-1 just freed; the global->LDS copy of tile kt+2 is in flight
+    //   from the barrier after step 0 to the next iteration's barrier.
     const int nk = a.K >> 6;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        if (kt + 1 < nk) gload((kt + 1) << 6);
-        const char* As = smem + (kt & 1) * T::STAGE;
-        const char* Bs = As + T::A_BYTES;
+    bf16x8 ra[4][T::TM], rb[4][T::TN];
+    auto read_frags = [&](const char* As, const char* Bs, int ks) {
+        const int c = ks * 2 + (lane >> 5);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const int c = ks * 2 + (lane >> 5);
-            bf16x8 af[T::TM], bfr[T::TN];
+        for (int i = 0; i < T::TM; ++i)
+            ra[ks][i] = *reinterpret_cast<const bf16x8*>(As + swz(wm * T::WM + i * 32 + (lane & 31), c));
 #pragma unroll
-            for (int i = 0; i < T::TM; ++i)
-                af[i] = *reinterpret_cast<const bf16x8*>(As + swz(wm * T::WM + i * 32 + (lane & 31), c));
+        for (int j = 0; j < T::TN; ++j)
+            rb[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + swz(wn * T::WN + j * 32 + (lane & 31), c));
+    };
+    auto mfmas = [&](int ks) {
 #pragma unroll
-            for (int j = 0; j < T::TN; ++j)
-                bfr[j] = *reinterpret_cast<const bf16x8*>(Bs + swz(wn * T::WN + j * 32 + (lane & 31), c));
+        for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-            for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-                for (int j = 0; j < T::TN; ++j) acc[i][j] = mfma32x32x16(af[i], bfr[j], acc[i][j]);
-        }
-        if (kt + 1 < nk) lstore((kt + 1) & 1);
-        __syncthreads();
+            for (int j = 0; j < T::TN; ++j) acc[i][j] = mfma32x32x16(ra[ks][i], rb[ks][j], acc[i][j]);
+    };
+    constexpr int NR = T::TM + T::TN, NM = T::TM * T::TN;
+
+    issue(0, 0);
+    if (nk > 1) issue(64, 1);
+    if (nk > 1) {
+        // tile 0 landed when at most tile 1's loads are still outstanding
+        wait_vmcnt<A_INSTR + B_INSTR>();
+    } else {
+        wait_all_memory();
     }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) read_frags(smem, smem + T::A_BYTES, ks);
+
+    for (int kt = 0; kt < nk; ++kt) {
+        mfmas(0);
+        wait_all_memory();                  // tile kt+1 (this wave's part) is in LDS
+        __syncthreads();                    // ... everyone's; nobody reads stage kt&1 any more
+        if (kt + 2 < nk) issue((kt + 2) << 6, kt & 1);
+        const char* As = smem + ((kt + 1) & 1) * T::STAGE;
+        const char* Bs = As + T::A_BYTES;
+        // (the last iteration reads fragments it never uses: in-bounds LDS reads
+        // keep the loop body free of branches so the reads interleave with MFMAs)
+#pragma unroll
+        for (int ks = 1; ks < 4; ++ks) {
+            mfmas(ks);
+            read_frags(As, Bs, ks - 1);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+                sched_group<0x008, (NM / NR > 0 ? NM / NR : 1)>();
+                sched_group<0x100, 1>();
+            }
+        }
+        read_frags(As, Bs, 3);
+    }
+    __syncthreads();                        // LDS is reused by the epilogues
 
     // ---------------------------------------------------------------- epilogues
     // acc[i][j][e] holds C[row][col] with
@@ -246,9 +307,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
             }
     } else if constexpr (EPI == EPI_QKV) {
         if (a.head_dim == 128)
-            qkv_epilogue<T::TM, T::TN, 128>(a, acc, m0, rows, n0, lrow0, lcol0);
+            qkv_epilogue<BM, BN, T::TM, T::TN, 128>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
         else
-            qkv_epilogue<T::TM, T::TN, 64>(a, acc, m0, rows, n0, lrow0, lcol0);
+            qkv_epilogue<BM, BN, T::TM, T::TN, 64>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
     } else if constexpr (EPI == EPI_LMHEAD) {
         // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
         // sum exp(z - max)) over this tile's BM vocabulary rows.

@@ -18,7 +18,7 @@ enum GemmEpilogue {
     EPI_F32 = 1,      // out_f32[row][col]
     EPI_RESID = 2,    // resid_f32[row][col] += acc
     EPI_SWIGLU = 3,   // out_bf16[row][f] = silu(gate) * up, gate/up interleaved in 32-col blocks
-    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K [B][KV][S][hd], Vt [B][KV][hd][S]
+    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K and V [B][KV][S][hd]
     EPI_LMHEAD = 5,   // rows = vocab, cols = tokens: per-(vocab tile, token) softmax partials
     EPI_F32_T = 6,    // out_f32[col][row] (transposed store)
 };
@@ -43,9 +43,9 @@ struct GemmArgs {
     // EPI_QKV
     bf16_t* q;
     bf16_t* k;
-    bf16_t* vt;
+    bf16_t* v;
     const float2* rope;       // [S][hd/2] (cos, sin)
-    int seq, seq_pad, n_heads, n_kv, head_dim;   // Vt rows are seq_pad long
+    int seq, n_heads, n_kv, head_dim;
     // EPI_LMHEAD: partials [M/BM tiles][N] (m, idx, s) stored as float4
     float4* partials;
 };
@@ -56,8 +56,8 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, bool grouped, int bm, int bn,
                        hipStream_t st);
 
 // ----------------------------------------------------------------- attention.hip
-// Non-causal attention; O [B*S][H*hd] bf16.
-hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, bf16_t* o, int B,
+// Non-causal attention over Q [B][H][S][hd], K, V [B][KV][S][hd]; O [B*S][H*hd] bf16.
+hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* v, bf16_t* o, int B,
                             int S, int H, int KV, int hd, hipStream_t st);
 
 // ----------------------------------------------------------------- elementwise.hip
@@ -82,16 +82,12 @@ void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int m
 void launch_zero_i32(int32_t* p, int n, hipStream_t st);
 
 // ----------------------------------------------------------------- moe.hip
-// Router softmax + top-k (ties -> lower id) + renormalisation; counts per expert.
-void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w,
-                 int32_t* counts, hipStream_t st);
-// Exclusive scan of counts (E routed + n_shared groups of T rows), tile table.
-void launch_dispatch_scan(int32_t* counts, int E, int n_shared, int T, int bm, int32_t* grp_off,
-                          int2* tile_tab, int32_t* n_tiles, int32_t* cursor, hipStream_t st);
-// Row permutation: slot[t][j] and a_rows[slot] = t.
-void launch_dispatch_scatter(const int32_t* ids, int T, int k, int E, int n_shared,
-                             const int32_t* grp_off, int32_t* cursor, int32_t* slot,
-                             int32_t* a_rows, hipStream_t st);
+// Router softmax + top-k (ties -> lower id) + renormalisation.
+void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w, hipStream_t st);
+// Group row ranges (E routed + n_shared groups of T rows), tile table of the
+// grouped GEMM (tile height bm), slot[t][j] and a_rows[row] = token.
+void launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared, int bm, int32_t* grp_off,
+                     int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows, hipStream_t st);
 // x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[shared rows]
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
                     const int32_t* grp_off, int T, int k, int E, int n_shared, int d,

@@ -10,8 +10,7 @@ namespace {
 // logits are selected (ties -> lower expert id) and their probabilities are
 // renormalised to sum to one.
 __global__ void topk_kernel(const float* __restrict__ logits, int T, int E, int k,
-                            int32_t* __restrict__ ids, float* __restrict__ w,
-                            int32_t* __restrict__ counts) {
+                            int32_t* __restrict__ ids, float* __restrict__ w) {
     const int lane = threadIdx.x & 63;
     const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (t >= T) return;
@@ -63,22 +62,29 @@ __global__ void topk_kernel(const float* __restrict__ logits, int T, int E, int 
         for (int r = 0; r < k; ++r) {
             ids[(int64_t)t * k + r] = isel[r];
             w[(int64_t)t * k + r] = psel[r] / psum;
-            atomicAdd(&counts[isel[r]], 1);
         }
     }
 }
 
-// Groups: E routed experts (rows = their counts) then n_shared shared experts
-// (T rows each).  Writes grp_off[0..G], the tile table (group, m0) and its
-// length, clears the scatter cursors, and re-zeroes counts for the next layer.
-__global__ void dispatch_scan_kernel(int32_t* __restrict__ counts, int E, int n_shared, int T, int bm,
-                                     int32_t* __restrict__ grp_off, int2* __restrict__ tile_tab,
-                                     int32_t* __restrict__ n_tiles, int32_t* __restrict__ cursor) {
+// One workgroup (1024 threads) builds the whole dispatch from the top-k ids:
+// groups are the E routed experts (rows = tokens routed there) followed by
+// n_shared shared experts (T rows each).  Writes grp_off[0..G], the tile table
+// (group, m0) of the grouped GEMM and its length, slot[t][j] (the row of
+// token t's j-th expert) and a_rows[row] = token.  Histogram and cursors live
+// in LDS; the row order inside a group depends on atomic order but no result
+// does (rows are computed independently and combined by slot).
+__global__ __launch_bounds__(1024) void dispatch_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                        int n_shared, int bm, int32_t* __restrict__ grp_off,
+                                                        int2* __restrict__ tile_tab, int32_t* __restrict__ n_tiles,
+                                                        int32_t* __restrict__ slot, int32_t* __restrict__ a_rows) {
     __shared__ int cnt[512];
     __shared__ int off[513];
     __shared__ int toff[513];
     const int G = E + n_shared;
-    for (int g = threadIdx.x; g < G; g += blockDim.x) cnt[g] = (g < E) ? counts[g] : T;
+    const int nr = T * k;
+    for (int g = threadIdx.x; g < G; g += blockDim.x) cnt[g] = (g < E) ? 0 : T;
+    __syncthreads();
+    for (int i = threadIdx.x; i < nr; i += blockDim.x) atomicAdd(&cnt[ids[i]], 1);
     __syncthreads();
     if (threadIdx.x == 0) {
         int o = 0, to = 0;
@@ -96,30 +102,20 @@ __global__ void dispatch_scan_kernel(int32_t* __restrict__ counts, int E, int n_
     __syncthreads();
     for (int g = threadIdx.x; g < G; g += blockDim.x) {
         grp_off[g] = off[g];
-        cursor[g] = 0;
-        if (g < E) counts[g] = 0;
         const int nt = toff[g + 1] - toff[g];
         for (int t = 0; t < nt; ++t) tile_tab[toff[g] + t] = make_int2(g, t * bm);
+        cnt[g] = 0;                                   // reused as the per-group cursor
     }
-}
-
-__global__ void dispatch_scatter_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
-                                        int n_shared, const int32_t* __restrict__ grp_off,
-                                        int32_t* __restrict__ cursor, int32_t* __restrict__ slot,
-                                        int32_t* __restrict__ a_rows) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    const int nr = T * k;
-    if (i < nr) {
-        const int t = i / k;
+    __syncthreads();
+    for (int i = threadIdx.x; i < nr; i += blockDim.x) {
         const int e = ids[i];
-        const int pos = atomicAdd(&cursor[e], 1);
-        const int s = grp_off[e] + pos;
+        const int s = off[e] + atomicAdd(&cnt[e], 1);
         slot[i] = s;
-        a_rows[s] = t;
-    } else if (i < nr + n_shared * T) {
-        const int i2 = i - nr;
-        const int sh = i2 / T, t = i2 - sh * T;
-        a_rows[grp_off[E + sh] + t] = t;
+        a_rows[s] = i / k;
+    }
+    for (int i = threadIdx.x; i < n_shared * T; i += blockDim.x) {
+        const int sh = i / T, t = i - sh * T;
+        a_rows[off[E + sh] + t] = t;
     }
 }
 
@@ -166,23 +162,14 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
 
 }  // namespace
 
-void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w, int32_t* counts,
-                 hipStream_t st) {
-    hipLaunchKernelGGL(topk_kernel, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, k, ids, w, counts);
+void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w, hipStream_t st) {
+    hipLaunchKernelGGL(topk_kernel, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, k, ids, w);
 }
 
-void launch_dispatch_scan(int32_t* counts, int E, int n_shared, int T, int bm, int32_t* grp_off,
-                          int2* tile_tab, int32_t* n_tiles, int32_t* cursor, hipStream_t st) {
-    hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(256), 0, st, counts, E, n_shared, T, bm,
-                       grp_off, tile_tab, n_tiles, cursor);
-}
-
-void launch_dispatch_scatter(const int32_t* ids, int T, int k, int E, int n_shared,
-                             const int32_t* grp_off, int32_t* cursor, int32_t* slot, int32_t* a_rows,
-                             hipStream_t st) {
-    const int n = T * k + n_shared * T;
-    hipLaunchKernelGGL(dispatch_scatter_kernel, dim3((n + 255) / 256), dim3(256), 0, st, ids, T, k, E,
-                       n_shared, grp_off, cursor, slot, a_rows);
+void launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared, int bm, int32_t* grp_off,
+                     int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows, hipStream_t st) {
+    hipLaunchKernelGGL(dispatch_kernel, dim3(1), dim3(1024), 0, st, ids, T, k, E, n_shared, bm, grp_off,
+                       tile_tab, n_tiles, slot, a_rows);
 }
 
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,

@@ -165,3 +165,16 @@ class Refiner:
         if n < 0:
             raise _lib.DlmError("dlm_profile_read failed")
         return [(names[i].decode(), float(ms[i])) for i in range(n)]
+
+
+# ------------------------------------------------------------------ GEMM hook
+
+def debug_gemm(a: torch.Tensor, b: torch.Tensor, tile=(256, 256)) -> torch.Tensor:
+    """float32 a @ b.T through the library's bf16 MFMA GEMM (a [m,k], b [n,k] bf16)."""
+    lib = _lib.load()
+    m, k = a.shape
+    n = b.shape[0]
+    c = torch.empty(m, n, dtype=torch.float32, device=a.device)
+    check(lib.dlm_debug_gemm(a.data_ptr(), b.data_ptr(), c.data_ptr(), m, n, k, tile[0], tile[1],
+                             torch.cuda.current_stream(a.device).cuda_stream), "dlm_debug_gemm")
+    return c

@@ -1,0 +1,33 @@
+"""The library's bf16 MFMA GEMM on its own against a float32 PyTorch reference
+(exact bf16 operands, so the only difference is fp32 summation order)."""
+
+from __future__ import annotations
+
+import pytest
+
+from tests.gpu_util import log, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("m,n,k,tile", [
+    (256, 256, 64, (256, 256)),
+    (300, 200, 128, (256, 256)),      # ragged in m and n
+    (1000, 520, 512, (256, 128)),
+    (77, 600, 192, (128, 256)),
+    (513, 129, 256, (128, 128)),
+    (130, 70, 64, (128, 64)),
+    (1, 1, 64, (128, 64)),
+])
+def test_gemm_matches_fp32_reference(m, n, k, tile):
+    need_gpu()
+    import torch
+    from paper_2608_02625_amd.model import debug_gemm
+    g = torch.Generator(device="cpu").manual_seed(m * 131 + n * 7 + k)
+    a = torch.randn(m, k, generator=g).to(torch.bfloat16).cuda()
+    b = torch.randn(n, k, generator=g).to(torch.bfloat16).cuda()
+    c = debug_gemm(a, b, tile)
+    ref = a.float().cpu() @ b.float().cpu().T
+    err = ((c.cpu() - ref).abs().max() / ref.abs().max()).item()
+    log(f"[gemm {m}x{n}x{k} tile {tile}] max-abs-rel {err:.2e}")
+    assert err < 1e-5
