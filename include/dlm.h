@@ -173,6 +173,8 @@ dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32
 /* dlm_debug_gemm: the library's bf16 MFMA GEMM on its own (for tests and
  *   measurements): d_c float [m][n] = d_a bf16 [m][k] * d_b bf16 [n][k]^T, with a
  *   tile of tile_m x tile_n (256x256, 256x128, 128x256, 128x128 or 128x64);
+ *   tile_m >> 16 selects an alternative K pipeline (1: 256x256 with 32-wide K
+ *   steps and 4 stages, 128x128 with 3 stages, 256x128 with 2 stages);
  *   k must be a multiple of 64. */
 dlm_status dlm_debug_gemm(const void* d_a, const void* d_b, float* d_c, int32_t m, int32_t n,
                           int32_t k, int32_t tile_m, int32_t tile_n, void* hip_stream);

@@ -397,6 +397,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = a_rows;
         a.out = hexp;
         a.ldo = F;
+        a.variant = 2;
         TRY(gemm(x, "gemm_expert_gate_up", a, EPI_SWIGLU, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     {
@@ -408,6 +409,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = nullptr;
         a.out = y;
         a.ldo = d;
+        a.variant = 2;
         TRY(gemm(x, "gemm_expert_down", a, EPI_BF16, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d, x.st));
@@ -430,6 +432,7 @@ dlm_status run_head(Ctx& x, int32_t* top1, float* conf, float* maxlogit, float* 
     GemmArgs a = gemm_args(x.wt(x.m->plan.lm), c.d_model, hfin, c.d_model, c.vocab, x.R, c.d_model);
     a.partials = x.at<float4>(x.w.partials);
     a.group_m = 4;
+    a.variant = 2;
     TRY(gemm(x, "gemm_lm_head", a, EPI_LMHEAD, false, kHeadBM, kHeadBN, 0));
     LAUNCH(x, "lmhead_merge", launch_lmhead_merge(a.partials, x.w.n_vtiles, x.R, top1, conf, maxlogit, x.st));
     if (logits_out) {
@@ -631,7 +634,8 @@ dlm_status dlm_debug_gemm(const void* d_a, const void* d_b, float* d_c, int32_t 
     GemmArgs a = gemm_args((const bf16_t*)d_a, k, (const bf16_t*)d_b, k, m, n, k);
     a.out = d_c;
     a.ldo = n;
-    hipError_t e = launch_gemm(a, EPI_F32, false, tile_m, tile_n, 0, (hipStream_t)hip_stream);
+    a.variant = tile_m >> 16;
+    hipError_t e = launch_gemm(a, EPI_F32, false, tile_m & 0xffff, tile_n, 0, (hipStream_t)hip_stream);
     if (e != hipSuccess) return fail(DLM_ERR_INVALID_ARG, std::string("gemm: ") + hipGetErrorString(e));
     return DLM_OK;
 }

@@ -23,19 +23,35 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int BM, int BN>
+template <int BM, int BN, int BK, int STAGES, int NW>
 struct TileCfg {
-    static constexpr int WM = BM / 2, WN = BN / 2;
+    static constexpr int NT = NW * 64;                   // threads
+    static constexpr int WM = BM / 2, WN = BN / (NW / 2);
     static constexpr int TM = WM / 32, TN = WN / 32;
-    static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
+    static constexpr int ROW = BK * 2;                   // bytes per LDS tile row
+    static constexpr int CPR = BK / 8;                   // 16-byte chunks per row
+    static constexpr int KS = BK / 16;                   // MFMA K steps per tile
+    static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
     static constexpr int STAGE = A_BYTES + B_BYTES;
-    static constexpr int LDS = 2 * STAGE;
+    static constexpr int LDS = STAGES * STAGE;
+    static constexpr int A_INSTR = A_BYTES / 1024 / NW;  // 1 KB DMA blocks per wave
+    static constexpr int B_INSTR = B_BYTES / 1024 / NW;
+    static constexpr int NI = A_INSTR + B_INSTR;         // DMA instructions per wave per tile
 };
 
-__device__ __forceinline__ int swz_key(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+// XOR key of the 16-byte chunks of a tile row: consecutive rows read by one
+// MFMA fragment land in distinct LDS banks (checked: no bank conflicts).
+template <int CPR>
+__device__ __forceinline__ int swz_key(int row) {
+    if constexpr (CPR == 8) return (row & 7) ^ ((row >> 3) & 1);
+    else return ((row >> 1) & 3) ^ ((row >> 3) & 1);
+}
 
-// Byte offset of logical 16-byte chunk `chunk` of tile row `row` (128-byte rows).
-__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ swz_key(row)) << 4); }
+// Byte offset of logical 16-byte chunk `chunk` of tile row `row`.
+template <int CPR>
+__device__ __forceinline__ int swz(int row, int chunk) {
+    return row * (CPR * 16) + ((chunk ^ swz_key<CPR>(row)) << 4);
+}
 
 // QKV projection epilogue: RoPE (rotate-half) on the q and k columns, then
 // Q [B][H][S][hd], K and V [B][KV][S][hd] stored row-major.  A wave's column
@@ -48,7 +64,7 @@ struct QkvEpi {
     static constexpr int LDS = BM * CS;
 };
 
-template <int BM, int BN, int TM, int TN, int HD>
+template <int BM, int BN, int TM, int TN, int HD, int NT>
 __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int rows,
                                              int n0, int lrow0, int lcol0, char* smem) {
     constexpr int HALF = HD / 2, SPT = HD / 32, POFF = HD / 64;
@@ -81,7 +97,7 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
         }
     __syncthreads();
     constexpr int CPR = BN / 8;                  // 16-byte chunks per row
-    for (int q = threadIdx.x; q < BM * CPR; q += 256) {
+    for (int q = threadIdx.x; q < BM * CPR; q += NT) {
         const int rl = q / CPR, ch = q - rl * CPR;
         const int row = m0 + rl;
         const int c = n0 + ch * 8;
@@ -106,14 +122,14 @@ constexpr int epi_lds() {
     return EPI == EPI_QKV ? QkvEpi<BM, BN, 128>::LDS : 0;
 }
 
-template <int BM, int BN, int EPI, bool GROUPED>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
-    using T = TileCfg<BM, BN>;
+template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void gemm_kernel(GemmArgs a) {
+    using T = TileCfg<BM, BN, BK, STAGES, NW>;
     constexpr int LDS_BYTES = T::LDS > epi_lds<BM, BN, EPI>() ? T::LDS : epi_lds<BM, BN, EPI>();
     __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / (NW / 2), wn = wave % (NW / 2);
     const int tiles_n = (a.N + BN - 1) / BN;
 
     // ---------------------------------------------------------------- tile decode
@@ -155,38 +171,38 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 
     // ---------------------------------------------------------------- main loop
     // Operands go global -> LDS directly (global_load_lds_dwordx4): one
-    // instruction per wave fills a contiguous 1 KB block = 8 tile rows of 128 B,
-    // lane L writing bytes [16L, 16L+16).  The XOR swizzle of the 16-byte
-    // chunks is applied on the global side: the lane that fills physical chunk
-    // pc of row r fetches logical chunk pc ^ f(r).
-    constexpr int A_INSTR = BM / 32, B_INSTR = BN / 32;        // 1 KB blocks per wave
+    // instruction per wave fills a contiguous 1 KB block of tile rows, lane L
+    // writing bytes [16L, 16L+16).  The XOR swizzle of the 16-byte chunks is
+    // applied on the global side: the lane that fills physical chunk pc of
+    // row r fetches logical chunk pc ^ key(r).
+    constexpr int CPR = T::CPR;
+    constexpr int RPB = 64 / CPR;                               // tile rows per 1 KB block
     const int wv = uniform(wave);
-    const int rin = lane >> 3, pc = lane & 7;
-    const bf16_t* a_src[A_INSTR];
-    const bf16_t* b_src[B_INSTR];
+    const int rin = lane / CPR, pc = lane % CPR;
+    const bf16_t* a_src[T::A_INSTR];
+    const bf16_t* b_src[T::B_INSTR];
 #pragma unroll
-    for (int p = 0; p < A_INSTR; ++p) {
-        const int tr = (wv * A_INSTR + p) * 8 + rin;               // row within the tile
+    for (int p = 0; p < T::A_INSTR; ++p) {
+        const int tr = (wv * T::A_INSTR + p) * RPB + rin;         // row within the tile
         const int r = min(m0 + tr, rows - 1);
         int64_t grow = r;
         if (GROUPED) grow = a.a_rows ? a.a_rows[row_base + r] : row_base + r;
-        a_src[p] = a.A + grow * a.lda + (pc ^ swz_key(tr)) * 8;
+        a_src[p] = a.A + grow * a.lda + (pc ^ swz_key<CPR>(tr)) * 8;
     }
 #pragma unroll
-    for (int p = 0; p < B_INSTR; ++p) {
-        const int tr = (wv * B_INSTR + p) * 8 + rin;
+    for (int p = 0; p < T::B_INSTR; ++p) {
+        const int tr = (wv * T::B_INSTR + p) * RPB + rin;
         const int n = min(n0 + tr, a.N - 1);
-        b_src[p] = Bg + (int64_t)n * a.ldb + (pc ^ swz_key(tr)) * 8;
+        b_src[p] = Bg + (int64_t)n * a.ldb + (pc ^ swz_key<CPR>(tr)) * 8;
     }
-    auto issue = [&](int k0, int stage) {
+    auto issue = [&](int kt, int stage) {
         char* As = smem + stage * T::STAGE;
         char* Bs = As + T::A_BYTES;
+        const int k0 = kt * BK;
 #pragma unroll
-        for (int p = 0; p < A_INSTR; ++p)
-            lds_dma16(a_src[p] + k0, As + (wv * A_INSTR + p) * 1024);
+        for (int p = 0; p < T::A_INSTR; ++p) lds_dma16(a_src[p] + k0, As + (wv * T::A_INSTR + p) * 1024);
 #pragma unroll
-        for (int p = 0; p < B_INSTR; ++p)
-            lds_dma16(b_src[p] + k0, Bs + (wv * B_INSTR + p) * 1024);
+        for (int p = 0; p < T::B_INSTR; ++p) lds_dma16(b_src[p] + k0, Bs + (wv * T::B_INSTR + p) * 1024);
     };
 
     f32x16 acc[T::TM][T::TN];
@@ -197,21 +213,22 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    // Software pipeline (per 64-wide K tile kt, LDS stage kt&1):
-    //   registers R hold all fragments of tile kt; the MFMAs of step ks run
-    //   while the fragments of tile kt+1 step ks-1 are read into the slot that
-    //   step ks-1 just freed; the global->LDS copy of tile kt+2 is in flight
-    //   from the barrier after step 0 to the next iteration's barrier.
-    const int nk = a.K >> 6;
-    bf16x8 ra[4][T::TM], rb[4][T::TN];
+    // Software pipeline over K tiles (tile kt lives in LDS stage kt % STAGES):
+    //   registers hold every fragment of tile kt; the MFMAs of step ks run while
+    //   the fragments of tile kt+1 step ks-1 are read into the slot step ks-1
+    //   just freed.  Tiles kt+1 .. kt+STAGES are in flight or landed; after the
+    //   barrier of iteration kt the copy of tile kt+STAGES goes into the stage
+    //   tile kt left.
+    const int nk = a.K / BK;
+    bf16x8 ra[T::KS][T::TM], rb[T::KS][T::TN];
     auto read_frags = [&](const char* As, const char* Bs, int ks) {
         const int c = ks * 2 + (lane >> 5);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
-            ra[ks][i] = *reinterpret_cast<const bf16x8*>(As + swz(wm * T::WM + i * 32 + (lane & 31), c));
+            ra[ks][i] = *reinterpret_cast<const bf16x8*>(As + swz<CPR>(wm * T::WM + i * 32 + (lane & 31), c));
 #pragma unroll
         for (int j = 0; j < T::TN; ++j)
-            rb[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + swz(wn * T::WN + j * 32 + (lane & 31), c));
+            rb[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + swz<CPR>(wn * T::WN + j * 32 + (lane & 31), c));
     };
     auto mfmas = [&](int ks) {
 #pragma unroll
@@ -221,39 +238,51 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     };
     constexpr int NR = T::TM + T::TN, NM = T::TM * T::TN;
 
-    issue(0, 0);
-    if (nk > 1) issue(64, 1);
-    if (nk > 1) {
-        // tile 0 landed when at most tile 1's loads are still outstanding
-        wait_vmcnt<A_INSTR + B_INSTR>();
-    } else {
-        wait_all_memory();
-    }
+#pragma unroll
+    for (int t = 0; t < STAGES; ++t)
+        if (t < nk) issue(t, t);
+    if (nk >= STAGES) wait_vmcnt<(STAGES - 1) * T::NI>();   // tile 0 landed, later tiles may fly
+    else wait_all_memory();
     __syncthreads();
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) read_frags(smem, smem + T::A_BYTES, ks);
+    for (int ks = 0; ks < T::KS; ++ks) read_frags(smem, smem + T::A_BYTES, ks);
 
     for (int kt = 0; kt < nk; ++kt) {
         mfmas(0);
-        wait_all_memory();                  // tile kt+1 (this wave's part) is in LDS
-        __syncthreads();                    // ... everyone's; nobody reads stage kt&1 any more
-        if (kt + 2 < nk) issue((kt + 2) << 6, kt & 1);
-        const char* As = smem + ((kt + 1) & 1) * T::STAGE;
+        if (kt + STAGES - 1 < nk) wait_vmcnt<(STAGES - 2) * T::NI>();   // tile kt+1 landed
+        else wait_all_memory();
+        __syncthreads();                    // everyone's tile kt+1 landed; stage of tile kt is free
+        const char* As = smem + ((kt + 1) % STAGES) * T::STAGE;
         const char* Bs = As + T::A_BYTES;
-        // (the last iteration reads fragments it never uses: in-bounds LDS reads
-        // keep the loop body free of branches so the reads interleave with MFMAs)
+        // Step 1 also issues the copy of tile kt+STAGES into the freed stage
+        // (past the end of K the last tile is copied again: the stage is never
+        // read, and the copy keeps the body free of branches so the copies and
+        // fragment reads interleave with the MFMAs).  The last iteration reads
+        // fragments it never uses, likewise harmless in-bounds LDS reads.
 #pragma unroll
-        for (int ks = 1; ks < 4; ++ks) {
+        for (int ks = 1; ks < T::KS; ++ks) {
             mfmas(ks);
+            if (ks == 1) issue(min(kt + STAGES, nk - 1), kt % STAGES);
             read_frags(As, Bs, ks - 1);
+            if (ks == 1) {
 #pragma unroll
-            for (int r = 0; r < NR; ++r) {
-                sched_group<0x008, (NM / NR > 0 ? NM / NR : 1)>();
-                sched_group<0x100, 1>();
+                for (int r = 0; r < T::NI; ++r) {
+                    sched_group<0x008, 1>();
+                    sched_group<0x020, 1>();     // one global->LDS copy
+                    if (r < NR) sched_group<0x100, 1>();
+                }
+                if (NM > T::NI) sched_group<0x008, (NM > T::NI ? NM - T::NI : 1)>();
+            } else {
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    sched_group<0x008, (NM / NR > 0 ? NM / NR : 1)>();
+                    sched_group<0x100, 1>();
+                }
             }
         }
-        read_frags(As, Bs, 3);
+        read_frags(As, Bs, T::KS - 1);
     }
+    wait_all_memory();
     __syncthreads();                        // LDS is reused by the epilogues
 
     // ---------------------------------------------------------------- epilogues
@@ -307,9 +336,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
             }
     } else if constexpr (EPI == EPI_QKV) {
         if (a.head_dim == 128)
-            qkv_epilogue<BM, BN, T::TM, T::TN, 128>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
+            qkv_epilogue<BM, BN, T::TM, T::TN, 128, T::NT>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
         else
-            qkv_epilogue<BM, BN, T::TM, T::TN, 64>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
+            qkv_epilogue<BM, BN, T::TM, T::TN, 64, T::NT>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
     } else if constexpr (EPI == EPI_LMHEAD) {
         // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
         // sum exp(z - max)) over this tile's BM vocabulary rows.
@@ -371,7 +400,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     }
 }
 
-template <int BM, int BN, int EPI, bool GROUPED>
+template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
 hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     const int tiles_n = (a.N + BN - 1) / BN;
     const int tiles_m = GROUPED ? max_tiles : (a.M + BM - 1) / BM;
@@ -379,17 +408,30 @@ hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     blocks = (blocks + 7) / 8 * 8;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, EPI, GROUPED>), dim3((unsigned)blocks), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, STAGES, NW, EPI, GROUPED>), dim3((unsigned)blocks), dim3(NW * 64), 0, st, a);
     return hipGetLastError();
 }
 
+// Tile configurations: BM x BN x BK with STAGES LDS stages (1 workgroup/CU
+// for the 256-row tiles; 128x128 and 128x64 leave room for two).
 template <int EPI, bool GROUPED>
 hipError_t launch_tiles(const GemmArgs& a, int bm, int bn, int max_tiles, hipStream_t st) {
-    if (bm == 256 && bn == 256) return launch_t<256, 256, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 256 && bn == 128) return launch_t<256, 128, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 256) return launch_t<128, 256, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 128) return launch_t<128, 128, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 64) return launch_t<128, 64, EPI, GROUPED>(a, max_tiles, st);
+    if (a.variant == 1) {
+        if (bm == 256 && bn == 256) return launch_t<256, 256, 32, 4, 4, EPI, GROUPED>(a, max_tiles, st);
+        if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 3, 4, EPI, GROUPED>(a, max_tiles, st);
+        if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+        return hipErrorInvalidValue;
+    }
+    if (a.variant == 2) {
+        if (EPI == EPI_QKV) return hipErrorInvalidValue;   // RoPE pairs must stay inside one wave
+        if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 8, EPI, GROUPED>(a, max_tiles, st);
+        return hipErrorInvalidValue;
+    }
+    if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 3, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 256) return launch_t<128, 256, 64, 3, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 64) return launch_t<128, 64, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
     return hipErrorInvalidValue;
 }
 

@@ -37,6 +37,7 @@ struct GemmArgs {
     const int* grp_off;       // [groups+1] row offsets (exclusive scan of group sizes)
     const int* a_rows;        // optional gather: A row of permuted row r (NULL = identity)
     int group_m;              // raster: m-tiles per raster group (dense mode)
+    int variant;              // K-pipeline variant (0 default; 1 alternative stage/BK choice)
     // epilogue
     void* out;
     int64_t ldo;
