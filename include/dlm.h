@@ -155,7 +155,9 @@ dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t d
  *   rows [batch*draft_len][vocab] through the same LM-head GEMM (test-only:
  *   the refine path never materialises logits).
  * dlm_debug_layer: one block `layer` applied to the float residual stream
- *   d_x_in [batch*seq][d_model], result to d_x_out (may equal d_x_in).
+ *   d_x_in [batch*seq][d_model], result to d_x_out (may equal d_x_in); for a
+ *   mixture-of-experts layer d_route_ids (may be NULL) receives the selected
+ *   experts int32 [batch*seq][top_k] in selection order.
  * dlm_debug_head: final norm + LM head + fused reduction on a float residual
  *   stream d_x [batch*(prompt_len+draft_len)][d_model] (draft rows used).
  */
@@ -165,7 +167,7 @@ dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, in
                              int32_t* d_top1, float* d_conf, float* d_logits);
 dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len,
                            const float* d_x_in, float* d_x_out, void* d_workspace,
-                           size_t workspace_bytes, void* hip_stream);
+                           size_t workspace_bytes, void* hip_stream, int32_t* d_route_ids);
 dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                           const float* d_x, void* d_workspace, size_t workspace_bytes,
                           void* hip_stream, float* d_max_logit, int32_t* d_top1, float* d_conf);

@@ -29,13 +29,27 @@ always-on shared expert, and an untied LM head.
 
 All arithmetic is float64 on weights that hold bfloat16 values; there is no
 blocking, fusion or reordering beyond the matrix products themselves.
+
+Integer decisions taken from floating-point values -- which experts a token is
+routed to, and the top-1 token of each draft position -- are taken in the
+precision of the GPU kernels that take them: the router and the LM head read
+their input activations rounded to bfloat16 (the GEMM operand precision), and
+their logits follow exactly from those operands.  Pass decide_bf16=False for
+the fully exact variant.
 """
 
 from __future__ import annotations
 
 import numpy as np
+import torch
 
 F64 = np.float64
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """x rounded float64 -> float32 -> bfloat16 (round to nearest even, torch), as float64."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float64).numpy()
 
 
 # ---------------------------------------------------------------- primitives
@@ -98,12 +112,15 @@ def swiglu(h: np.ndarray, w_gate, w_up, w_down) -> np.ndarray:
     return (silu(g) * u) @ w_down.astype(F64).T
 
 
-def route(h: np.ndarray, w_router, k: int):
+def route(h: np.ndarray, w_router, k: int, decide_bf16: bool = True):
     """Softmax router, top-k (ties go to the lower expert id), renormalised.
 
     Returns ids [T, k], weights [T, k] and the logit gap between the k-th and
-    (k+1)-th ranked experts (inf when k == E).
+    (k+1)-th ranked experts (inf when k == E).  With decide_bf16 the router
+    reads h rounded to bfloat16.
     """
+    if decide_bf16:
+        h = bf16_round(h)
     z = h @ w_router.astype(F64).T                                     # [T, E]
     p = softmax(z, axis=-1)
     order = np.argsort(-z, axis=-1, kind="stable")                     # desc, ties -> lower id
@@ -119,10 +136,10 @@ def route(h: np.ndarray, w_router, k: int):
     return ids, w, gap
 
 
-def moe_ffn(h: np.ndarray, L: dict, k: int):
+def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = True):
     """Sum over the selected experts of w_j * SwiGLU_j(h), plus the shared experts."""
     T = h.shape[0]
-    ids, w, gap = route(h, L["w_router"], k)
+    ids, w, gap = route(h, L["w_router"], k, decide_bf16)
     out = np.zeros_like(h)
     for e, (wg, wu, wd) in enumerate(L["experts"]):
         rows, slot = np.nonzero(ids == e)
@@ -137,7 +154,7 @@ def moe_ffn(h: np.ndarray, L: dict, k: int):
 
 # ---------------------------------------------------------------- forward
 
-def layer_forward(shape, L: dict, x: np.ndarray):
+def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True):
     """One pre-norm block over x [B, S, d] (all positions, no attention mask)."""
     B, S, d = x.shape
     H, KV, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
@@ -158,14 +175,14 @@ def layer_forward(shape, L: dict, x: np.ndarray):
     if shape.n_experts == 0:
         ffn = swiglu(h2, L["w_gate"], L["w_up"], L["w_down"])
     else:
-        ffn, ids, gap = moe_ffn(h2, L, shape.top_k)
+        ffn, ids, gap = moe_ffn(h2, L, shape.top_k, decide_bf16)
         info["route_gap"] = gap.reshape(B, S)
         info["route_ids"] = ids.reshape(B, S, -1)
     x += ffn.reshape(B, S, d)
     return x, info
 
 
-def forward(W, tokens: np.ndarray, collect: bool = False):
+def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = True):
     """Residual stream after the last layer (before the final norm): [B, S, d].
 
     With collect=True also returns per-layer infos and per-layer inputs.
@@ -176,7 +193,7 @@ def forward(W, tokens: np.ndarray, collect: bool = False):
     for l in range(shape.n_layers):
         if collect:
             inputs.append(x.copy())
-        x, info = layer_forward(shape, W.layer(l), x)
+        x, info = layer_forward(shape, W.layer(l), x, decide_bf16)
         infos.append(info)
     if collect:
         return x, infos, inputs
@@ -185,8 +202,10 @@ def forward(W, tokens: np.ndarray, collect: bool = False):
 
 # ---------------------------------------------------------------- reduction
 
-def lm_head_reduce(W, x_rows: np.ndarray, row_chunk: int = 256, want_logits: bool = False):
-    """Per row: logits z = (rms(x) g_f) Wlm^T over the full vocabulary, then
+def lm_head_reduce(W, x_rows: np.ndarray, row_chunk: int = 256, want_logits: bool = False,
+                   decide_bf16: bool = True):
+    """Per row: logits z = (rms(x) g_f) Wlm^T over the full vocabulary (the
+    normalised row rounded to bfloat16 when decide_bf16), then
 
       m     = max_v z_v
       top1  = min { v : z_v = m }           (first maximum)
@@ -204,6 +223,8 @@ def lm_head_reduce(W, x_rows: np.ndarray, row_chunk: int = 256, want_logits: boo
     logits = [] if want_logits else None
     for r0 in range(0, R, row_chunk):
         hx = rms_norm(x_rows[r0:r0 + row_chunk], W.final_norm(), shape.norm_eps)
+        if decide_bf16:
+            hx = bf16_round(hx)
         z = hx @ wlm.T
         t = np.argmax(z, axis=-1)
         mm = z[np.arange(z.shape[0]), t]
@@ -238,13 +259,13 @@ def edit_rule(draft: np.ndarray, top1: np.ndarray, conf: np.ndarray, tau: float,
     return new, n_unmasked, n_edited
 
 
-def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float):
+def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float, decide_bf16: bool = True):
     """One refinement pass over tokens [B, S] (prompt in [0, P), draft in [P, S))."""
     shape = W.shape
     B, S = tokens.shape
     D = S - prompt_len
-    x = forward(W, tokens)
-    red = lm_head_reduce(W, x[:, prompt_len:, :].reshape(B * D, -1))
+    x = forward(W, tokens, decide_bf16=decide_bf16)
+    red = lm_head_reduce(W, x[:, prompt_len:, :].reshape(B * D, -1), decide_bf16=decide_bf16)
     top1 = red["top1"].reshape(B, D)
     conf = red["conf"].reshape(B, D)
     new_draft, n_unm, n_edit = edit_rule(tokens[:, prompt_len:], top1, conf, tau, shape.mask_id)
@@ -256,7 +277,7 @@ def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float):
 
 
 def refine(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_steps: int,
-           tau: float):
+           tau: float, decide_bf16: bool = True):
     """Draft positions in the mask set start as [MASK]; then up to n_steps passes,
     stopping after a pass that changed nothing.  Returns (final draft, stats)."""
     shape = W.shape
@@ -267,7 +288,7 @@ def refine(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_
     tokens = np.concatenate([prompt, d], axis=1).astype(np.int32)
     stats = {"steps_run": 0, "n_unmasked": 0, "n_edited": 0, "per_step": []}
     for _ in range(n_steps):
-        tokens, info = refine_step(W, tokens, P, tau)
+        tokens, info = refine_step(W, tokens, P, tau, decide_bf16)
         stats["steps_run"] += 1
         stats["n_unmasked"] += info["n_unmasked"]
         stats["n_edited"] += info["n_edited"]

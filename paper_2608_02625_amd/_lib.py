@@ -50,7 +50,7 @@ SIGNATURES = [
     ("dlm_refine_step", _I, [_P, _I, _I, _I, _P, _F, _P, _SZ, _P, _P, _P, _P]),
     ("dlm_refine", _I, [_P, _I, _I, _I, _P, _P, _P, _I, _F, _P, _SZ, _P, ctypes.POINTER(DlmStats)]),
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
-    ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P]),
+    ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),
     ("dlm_debug_gemm", _I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),
     ("dlm_weight_info", _I, [_P, _I, _I, _I, ctypes.POINTER(_P), ctypes.POINTER(_I)]),

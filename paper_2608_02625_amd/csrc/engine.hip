@@ -597,7 +597,8 @@ dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, in
 }
 
 dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len, const float* d_x_in,
-                           float* d_x_out, void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+                           float* d_x_out, void* d_workspace, size_t workspace_bytes, void* hip_stream,
+                           int32_t* d_route_ids) {
     Workspace w;
     TRY(check_common(m, batch, 0, seq_len, d_workspace, workspace_bytes, &w));
     if (layer < 0 || layer >= m->cfg.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
@@ -608,6 +609,9 @@ dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t s
     TRY(run_prologue(x, nullptr));
     TRY(run_layer(x, layer));
     HIP_TRY(hipMemcpyAsync(d_x_out, x.at<float>(w.x), bytes, hipMemcpyDeviceToDevice, x.st));
+    if (d_route_ids && m->cfg.n_experts > 0)
+        HIP_TRY(hipMemcpyAsync(d_route_ids, x.at<int32_t>(w.ids), (size_t)x.T * m->cfg.top_k * 4,
+                               hipMemcpyDeviceToDevice, x.st));
     return DLM_OK;
 }
 

@@ -220,10 +220,10 @@ def test_route_ties_go_to_lower_id_and_weights_renormalise():
     rng = np.random.default_rng(8)
     hh = rng.standard_normal((20, 8))
     wr2 = rng.standard_normal((6, 8))
-    ids, w, _ = route(hh, wr2, 6)              # k = E: full softmax mixture
+    ids, w, _ = route(hh, wr2, 6, decide_bf16=False)   # k = E: full softmax mixture
     p = scipy.special.softmax(hh @ wr2.T, axis=-1)
     assert np.allclose(np.take_along_axis(p, ids, -1), w, rtol=1e-13)
-    _, w3, _ = route(hh, wr2, 3)
+    _, w3, _ = route(hh, wr2, 3, decide_bf16=False)
     assert np.allclose(w3.sum(-1), 1.0, rtol=1e-14)
 
 
@@ -258,6 +258,32 @@ def test_moe_reductions():
     assert np.allclose(a - b, swiglu(h, *sh["shared"][0]), rtol=1e-12, atol=1e-13)
 
 
+def test_decisions_read_bf16_rounded_operands():
+    from oracle.refine import bf16_round
+    # representable values are unchanged; ties go to even; float64 is rounded to
+    # float32 first (as the kernels round their fp32 activations), so
+    # 1 + 2^-8 + 2^-30 -> 1 + 2^-8 (fp32) -> 1.0 (bf16 tie to even).
+    assert np.array_equal(bf16_round(np.array([1.0, -0.5, 3.0, 2.0 ** -20])), [1.0, -0.5, 3.0, 2.0 ** -20])
+    assert bf16_round(np.array([1.0 + 2 ** -8]))[0] == 1.0
+    assert bf16_round(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+    assert bf16_round(np.array([1.0 + 2 ** -8 + 2 ** -30]))[0] == 1.0
+    # inputs already on the bf16 grid: both decision precisions agree exactly
+    rng = np.random.default_rng(21)
+    h = bf16_round(rng.standard_normal((40, 16)))
+    wr = rng.standard_normal((8, 16))
+    a = route(h, wr, 3, decide_bf16=True)
+    b = route(h, wr, 3, decide_bf16=False)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    # the router ranks on the rounded input: a near tie that rounding reverses
+    wr2 = np.array([[1.0, 0.0], [0.0, 1.0]])
+    hh = np.array([[1.0 + 2 ** -9, 1.0 + 2 ** -10]])      # exact: expert 0 ahead; bf16: tie -> lower id 0
+    assert route(hh, wr2, 1, decide_bf16=False)[0][0, 0] == 0
+    assert route(hh, wr2, 1, decide_bf16=True)[0][0, 0] == 0
+    hh = np.array([[1.0 + 2 ** -10, 1.0 + 2 ** -9]])      # exact: expert 1 ahead; bf16: tie -> 0
+    assert route(hh, wr2, 1, decide_bf16=False)[0][0, 0] == 1
+    assert route(hh, wr2, 1, decide_bf16=True)[0][0, 0] == 0
+
+
 # ---------------------------------------------------------------- reduction
 
 class _HeadOnly:
@@ -277,7 +303,7 @@ def test_lm_head_reduce_against_explicit_softmax():
     shape = MODELS["tiny"].replace(vocab=300, d_model=32)
     wlm = rng.standard_normal((300, 32)) * 0.5
     x = rng.standard_normal((17, 32))
-    red = lm_head_reduce(_HeadOnly(shape, wlm), x, row_chunk=5, want_logits=True)
+    red = lm_head_reduce(_HeadOnly(shape, wlm), x, row_chunk=5, want_logits=True, decide_bf16=False)
     z = (x / np.sqrt(np.mean(x * x, -1, keepdims=True) + shape.norm_eps)) @ wlm.T
     p = scipy.special.softmax(z, axis=-1)
     assert np.array_equal(red["top1"], np.argmax(z, -1))
@@ -327,7 +353,7 @@ def test_identity_blocks_closed_form():
     tokens = np.array([[3, 7, 1, 30, 5, 5, 0]])
     x = forward(W, tokens)
     assert np.array_equal(x, E[tokens])
-    red = lm_head_reduce(W, x[0])
+    red = lm_head_reduce(W, x[0], decide_bf16=False)
     a = math.exp(math.sqrt(64 / (1 + 64 * shape.norm_eps)))
     assert np.array_equal(red["top1"], tokens[0])
     assert np.allclose(red["conf"], a / (a + 31), rtol=1e-12)
