@@ -111,6 +111,8 @@ def main():
     ap.add_argument("--kernel", default="gemm_expert_gate_up", help="kernel reported in roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-table", action="store_true", help="also time every kernel (separate pass)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (reference for memory counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); multi-GPU sharding is not built",
@@ -127,6 +129,14 @@ def main():
     shape = w.model
     B, P, D = w.batch, w.prompt_len, w.draft_len
     torch.cuda.set_device(0)
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     print(f"[bench] workload {w.name}: B={B} P={P} D={D}; loading synthetic weights", file=sys.stderr, flush=True)
     R = Refiner(shape.as_dict(), w.weight_seed)
     prompt, draft, mask = make_inputs(w)

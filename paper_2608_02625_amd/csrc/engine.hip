@@ -330,8 +330,9 @@ dlm_status run_layer(Ctx& x, int l) {
 
     LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g1), h, x.T, d, c.norm_eps, x.st));
     {
+        // Transposed: rows = the (H + 2 KV) * hd output features, columns = tokens.
         const int N = (H + 2 * KV) * hd;
-        GemmArgs a = gemm_args(h, d, x.wt(L.wqkv), d, x.T, N, d);
+        GemmArgs a = gemm_args(x.wt(L.wqkv), d, h, d, N, x.T, d);
         a.q = q;
         a.k = k;
         a.v = v;
@@ -340,7 +341,9 @@ dlm_status run_layer(Ctx& x, int l) {
         a.n_heads = H;
         a.n_kv = KV;
         a.head_dim = hd;
-        TRY(gemm(x, "gemm_qkv", a, EPI_QKV, false, x.T >= 4096 ? 256 : 128, 256, 0));
+        const int64_t big_tiles = (int64_t)((N + 255) / 256) * ((x.T + 255) / 256);
+        a.variant = big_tiles >= 192 ? 2 : 0;
+        TRY(gemm(x, "gemm_qkv", a, EPI_QKV, false, 256, a.variant == 2 ? 256 : 128, 0));
     }
     {
         prof_begin(x, "attention");
@@ -352,7 +355,10 @@ dlm_status run_layer(Ctx& x, int l) {
         GemmArgs a = gemm_args(attn, (int64_t)H * hd, x.wt(L.wo), (int64_t)H * hd, x.T, d, H * hd);
         a.out = xs;
         a.ldo = d;
-        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, x.T >= 4096 ? 256 : 128, 128, 0));
+        const int64_t big_tiles = (int64_t)((x.T + 255) / 256) * ((d + 255) / 256);
+        a.variant = big_tiles >= 128 ? 2 : 0;
+        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, a.variant == 2 || x.T >= 4096 ? 256 : 128,
+                 a.variant == 2 ? 256 : 128, 0));
     }
     LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g2), h, x.T, d, c.norm_eps, x.st));
     if (c.n_experts == 0) {

@@ -53,80 +53,63 @@ __device__ __forceinline__ int swz(int row, int chunk) {
     return row * (CPR * 16) + ((chunk ^ swz_key<CPR>(row)) << 4);
 }
 
-// QKV projection epilogue: RoPE (rotate-half) on the q and k columns, then
-// Q [B][H][S][hd], K and V [B][KV][S][hd] stored row-major.  A wave's column
-// range covers whole heads, so the rotation partners (i, i + hd/2) sit in the
-// same lane, subtiles j and j + hd/64.  The rotated tile is staged in LDS as
-// bf16 so that the stores are 16-byte row chunks.
-template <int BM, int BN, int HD>
-struct QkvEpi {
-    static constexpr int CS = BN * 2 + 16;       // LDS row stride (bytes)
-    static constexpr int LDS = BM * CS;
-};
-
-template <int BM, int BN, int TM, int TN, int HD, int NT>
-__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int rows,
-                                             int n0, int lrow0, int lcol0, char* smem) {
-    constexpr int HALF = HD / 2, SPT = HD / 32, POFF = HD / 64;
-    constexpr int CS = QkvEpi<BM, BN, HD>::CS;
+// QKV projection, computed transposed: rows = q/k/v features, columns =
+// tokens.  A lane then holds, per accumulator, 4 consecutive features of one
+// token (8-byte stores into Q [B][H][S][hd], K and V [B][KV][S][hd]), and a
+// wave's 128 rows cover whole heads, so the RoPE partners (i, i + hd/2) are in
+// the same lane, accumulator rows i and i + hd/64 (rotate-half, applied in
+// fp32 before rounding).
+template <int TM, int TN, int HD>
+__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int m0, int n0,
+                                             int lrow0, int lcol0) {
+    constexpr int HALF = HD / 2, SPH = HD / 32, POFF = HD / 64;
     const int Hq = a.n_heads * HD, Hk = a.n_kv * HD;
     const int S = a.seq;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int j = 0; j < TN; ++j) {
+        const int t = n0 + lcol0 + j * 32;                    // token
+        if (t >= a.N) continue;
+        const int b = t / S, s = t - b * S;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int rl = lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-            const int row = m0 + rl;
-            const int s = (row < rows) ? row % S : 0;
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int cl = lcol0 + j * 32;
-                const int c = n0 + cl;
-                float v = acc[i][j][e];
-                if (c < Hq + Hk) {
-                    if ((j % SPT) < POFF) {
-                        const float2 cs = a.rope[s * HALF + (c % HD)];
-                        v = v * cs.x - acc[i][(j + POFF) % TN][e] * cs.y;
+            for (int q = 0; q < 4; ++q) {
+                const int f0 = m0 + lrow0 + i * 32 + 8 * q;       // first of 4 consecutive features
+                if (f0 >= a.M) continue;                           // M is a multiple of HD
+                float v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+                bf16_t* dst;
+                if (f0 < Hq + Hk) {
+                    const int hi0 = f0 % HD;
+                    const float4* cs = reinterpret_cast<const float4*>(a.rope + s * HALF + (hi0 % HALF));
+                    const float4 c01 = cs[0], c23 = cs[1];          // (cos, sin) of 4 consecutive pairs
+                    const float cz[4] = {c01.x, c01.z, c23.x, c23.z};
+                    const float sn[4] = {c01.y, c01.w, c23.y, c23.w};
+                    if ((i % SPH) < POFF) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cz[r] - acc[(i + POFF) % TM][j][4 * q + r] * sn[r];
                     } else {
-                        const float2 cs = a.rope[s * HALF + (c % HD) - HALF];
-                        v = v * cs.x + acc[i][(j + TN - POFF) % TN][e] * cs.y;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cz[r] + acc[(i + TM - POFF) % TM][j][4 * q + r] * sn[r];
                     }
+                    if (f0 < Hq)
+                        dst = a.q + (((int64_t)b * a.n_heads + f0 / HD) * S + s) * HD + hi0;
+                    else
+                        dst = a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * S + s) * HD + hi0;
+                } else {
+                    const int fv = f0 - Hq - Hk;
+                    dst = a.v + (((int64_t)b * a.n_kv + fv / HD) * S + s) * HD + (fv % HD);
                 }
-                *reinterpret_cast<bf16_t*>(smem + rl * CS + cl * 2) = f32_to_bf16(v);
+                *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
             }
-        }
-    __syncthreads();
-    constexpr int CPR = BN / 8;                  // 16-byte chunks per row
-    for (int q = threadIdx.x; q < BM * CPR; q += NT) {
-        const int rl = q / CPR, ch = q - rl * CPR;
-        const int row = m0 + rl;
-        const int c = n0 + ch * 8;
-        if (row >= rows || c >= a.N) continue;
-        const int b = row / S, s = row - b * S;
-        bf16_t* dst;
-        if (c < Hq) {
-            dst = a.q + (((int64_t)b * a.n_heads + c / HD) * S + s) * HD + (c % HD);
-        } else if (c < Hq + Hk) {
-            const int ck = c - Hq;
-            dst = a.k + (((int64_t)b * a.n_kv + ck / HD) * S + s) * HD + (ck % HD);
-        } else {
-            const int cv = c - Hq - Hk;
-            dst = a.v + (((int64_t)b * a.n_kv + cv / HD) * S + s) * HD + (cv % HD);
-        }
-        *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(smem + rl * CS + ch * 16);
     }
-}
-
-template <int BM, int BN, int EPI>
-constexpr int epi_lds() {
-    return EPI == EPI_QKV ? QkvEpi<BM, BN, 128>::LDS : 0;
 }
 
 template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void gemm_kernel(GemmArgs a) {
     using T = TileCfg<BM, BN, BK, STAGES, NW>;
-    constexpr int LDS_BYTES = T::LDS > epi_lds<BM, BN, EPI>() ? T::LDS : epi_lds<BM, BN, EPI>();
-    __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+    __shared__ __attribute__((aligned(16))) char smem[T::LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / (NW / 2), wn = wave % (NW / 2);
@@ -335,10 +318,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                 }
             }
     } else if constexpr (EPI == EPI_QKV) {
+        static_assert(T::WM % 128 == 0, "a wave's rows must cover whole heads");
         if (a.head_dim == 128)
-            qkv_epilogue<BM, BN, T::TM, T::TN, 128, T::NT>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
+            qkv_epilogue<T::TM, T::TN, 128>(a, acc, m0, n0, lrow0, lcol0);
         else
-            qkv_epilogue<BM, BN, T::TM, T::TN, 64, T::NT>(a, acc, m0, rows, n0, lrow0, lcol0, smem);
+            qkv_epilogue<T::TM, T::TN, 64>(a, acc, m0, n0, lrow0, lcol0);
     } else if constexpr (EPI == EPI_LMHEAD) {
         // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
         // sum exp(z - max)) over this tile's BM vocabulary rows.
@@ -402,6 +386,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
 
 template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
 hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
+    if constexpr (EPI == EPI_QKV && (BM / 2) % 128 != 0) {
+        return hipErrorInvalidValue;                       // RoPE pairs must stay inside one wave
+    } else {
     const int tiles_n = (a.N + BN - 1) / BN;
     const int tiles_m = GROUPED ? max_tiles : (a.M + BM - 1) / BM;
     int64_t blocks = (int64_t)tiles_m * tiles_n;
@@ -410,6 +397,7 @@ hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, STAGES, NW, EPI, GROUPED>), dim3((unsigned)blocks), dim3(NW * 64), 0, st, a);
     return hipGetLastError();
+    }
 }
 
 // Tile configurations: BM x BN x BK with STAGES LDS stages (1 workgroup/CU
@@ -423,7 +411,6 @@ hipError_t launch_tiles(const GemmArgs& a, int bm, int bn, int max_tiles, hipStr
         return hipErrorInvalidValue;
     }
     if (a.variant == 2) {
-        if (EPI == EPI_QKV) return hipErrorInvalidValue;   // RoPE pairs must stay inside one wave
         if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 8, EPI, GROUPED>(a, max_tiles, st);
         return hipErrorInvalidValue;
     }
