@@ -40,6 +40,37 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
     __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)lds, 16, 0, 0);
 #endif
 }
+// Raw buffer resource over a byte range starting at `base` (wave-uniform):
+// loads address base + voffset + soffset, with 32-bit offsets.
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef __amdgpu_buffer_rsrc_t buf_rsrc_t;
+#else
+struct buf_rsrc_t {
+    uint32_t w[4];
+};
+#endif
+__device__ __forceinline__ buf_rsrc_t make_rsrc(const void* base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+#else
+    return buf_rsrc_t{};
+#endif
+}
+// Buffer form of lds_dma16: lane L reads 16 bytes at voffset(L) + soffset and
+// writes them to bytes [16L, 16L+16) of the LDS block at `lds`.
+__device__ __forceinline__ void lds_dma16_buf(buf_rsrc_t r, uint32_t voffset, int soffset, lds_ptr_t lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, (int)voffset, soffset, 0, 0);
+#endif
+}
+// Wait until at most N LDS operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_lgkmcnt() {
+    static_assert(N >= 0 && N < 16, "lgkmcnt range");
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
+#endif
+}
 // Wait until every outstanding memory operation of this wave has completed.
 __device__ __forceinline__ void wait_all_memory() {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -67,6 +98,13 @@ template <int MASK, int N>
 __device__ __forceinline__ void sched_group() {
 #if defined(__HIP_DEVICE_COMPILE__)
     __builtin_amdgcn_sched_group_barrier(MASK, N, 0);
+#endif
+}
+
+// Scheduling fence: the compiler moves no instruction across it.
+__device__ __forceinline__ void sched_fence() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_sched_barrier(0);
 #endif
 }
 

@@ -1,13 +1,13 @@
 // bf16 MFMA GEMM for gfx950 with fused epilogues.
 //
 // C[M x N] = A[M x K] * B[N x K]^T, fp32 accumulation, both operands K-contiguous.
-// A workgroup of 256 threads (4 waves in a 2x2 grid) owns a BM x BN tile; each
-// wave owns (BM/2) x (BN/2) as a grid of 32x32 accumulators fed by
-// v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through two LDS stages:
-// the global->LDS loads of stage k+1 (direct to LDS, no register staging) are
-// in flight while the MFMAs of stage k run.
-// LDS rows are 128 bytes (64 bf16) with 16-byte chunks XOR-swizzled by row
-// bits so that fragment reads of 32 consecutive rows spread over all banks.
+// A workgroup owns a BM x BN tile: 4 waves in a 2x2 grid or 8 waves in a 2x4
+// grid (two per SIMD), each wave a grid of 32x32 accumulators fed by
+// v_mfma_f32_32x32x16_bf16.  K advances BK at a time through LDS stages filled
+// straight from global memory by buffer loads (no register staging) while the
+// MFMAs of earlier K tiles run.
+// LDS rows are BK*2 bytes with 16-byte chunks XOR-swizzled by row bits so that
+// fragment reads of 32 consecutive rows spread over all banks.
 //
 // Grouped mode runs one GEMM per expert over a device-built tile table; the A
 // rows of a group may be gathered through an index array (token -> expert
@@ -153,39 +153,50 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const bf16_t* Bg = a.B + (GROUPED ? (int64_t)g * a.b_group_stride : 0);
 
     // ---------------------------------------------------------------- main loop
-    // Operands go global -> LDS directly (global_load_lds_dwordx4): one
+    // Operands go global -> LDS directly (buffer_load_dwordx4 ... lds): one
     // instruction per wave fills a contiguous 1 KB block of tile rows, lane L
-    // writing bytes [16L, 16L+16).  The XOR swizzle of the 16-byte chunks is
-    // applied on the global side: the lane that fills physical chunk pc of
-    // row r fetches logical chunk pc ^ key(r).
+    // writing bytes [16L, 16L+16).  A lane's 32-bit byte offset into its
+    // operand is fixed for the whole K loop and K advances through the scalar
+    // offset, so the copies cost no vector ALU work.  The XOR swizzle of the
+    // 16-byte chunks is applied on the global side: the lane that fills
+    // physical chunk pc of row r fetches logical chunk pc ^ key(r).
+    // LDS = [A stage 0 .. A stage S-1 | B stage 0 .. B stage S-1]; fragment
+    // reads are a per-lane base plus a compile-time offset.
     constexpr int CPR = T::CPR;
     constexpr int RPB = 64 / CPR;                               // tile rows per 1 KB block
+    constexpr int B_BASE = STAGES * T::A_BYTES;
     const int wv = uniform(wave);
     const int rin = lane / CPR, pc = lane % CPR;
-    const bf16_t* a_src[T::A_INSTR];
-    const bf16_t* b_src[T::B_INSTR];
+    const bool gather = GROUPED && a.a_rows != nullptr;
+    const bf16_t* a_tile = gather ? a.A : a.A + (int64_t)uniform(row_base + m0) * a.lda;
+    const buf_rsrc_t a_rsrc = make_rsrc(a_tile);
+    const buf_rsrc_t b_rsrc = make_rsrc(Bg + (int64_t)n0 * a.ldb);
+    uint32_t a_off[T::A_INSTR], b_off[T::B_INSTR];
 #pragma unroll
     for (int p = 0; p < T::A_INSTR; ++p) {
         const int tr = (wv * T::A_INSTR + p) * RPB + rin;         // row within the tile
         const int r = min(m0 + tr, rows - 1);
-        int64_t grow = r;
-        if (GROUPED) grow = a.a_rows ? a.a_rows[row_base + r] : row_base + r;
-        a_src[p] = a.A + grow * a.lda + (pc ^ swz_key<CPR>(tr)) * 8;
+        const int64_t grow = gather ? (int64_t)a.a_rows[row_base + r] : (int64_t)(r - m0);
+        a_off[p] = (uint32_t)(grow * a.lda * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
     }
 #pragma unroll
     for (int p = 0; p < T::B_INSTR; ++p) {
         const int tr = (wv * T::B_INSTR + p) * RPB + rin;
-        const int n = min(n0 + tr, a.N - 1);
-        b_src[p] = Bg + (int64_t)n * a.ldb + (pc ^ swz_key<CPR>(tr)) * 8;
+        const int n = min(n0 + tr, a.N - 1) - n0;
+        b_off[p] = (uint32_t)((int64_t)n * a.ldb * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
     }
-    auto issue = [&](int kt, int stage) {
-        char* As = smem + stage * T::STAGE;
-        char* Bs = As + T::A_BYTES;
-        const int k0 = kt * BK;
+    const lds_ptr_t lds = (lds_ptr_t)smem;
+    typedef __attribute__((address_space(3))) char lds_char;
+    typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
+    auto lds_at = [&](int off) { return (lds_ptr_t)((lds_char*)lds + off); };
+    auto issue = [&](int kt, int stage) {                        // tile kt -> LDS stage
+        const int soff = kt * (BK * 2);
+        const int a_dst = stage * T::A_BYTES + wv * T::A_INSTR * 1024;
+        const int b_dst = B_BASE + stage * T::B_BYTES + wv * T::B_INSTR * 1024;
 #pragma unroll
-        for (int p = 0; p < T::A_INSTR; ++p) lds_dma16(a_src[p] + k0, As + (wv * T::A_INSTR + p) * 1024);
+        for (int p = 0; p < T::A_INSTR; ++p) lds_dma16_buf(a_rsrc, a_off[p], soff, lds_at(a_dst + p * 1024));
 #pragma unroll
-        for (int p = 0; p < T::B_INSTR; ++p) lds_dma16(b_src[p] + k0, Bs + (wv * T::B_INSTR + p) * 1024);
+        for (int p = 0; p < T::B_INSTR; ++p) lds_dma16_buf(b_rsrc, b_off[p], soff, lds_at(b_dst + p * 1024));
     };
 
     f32x16 acc[T::TM][T::TN];
@@ -196,22 +207,29 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    // Software pipeline over K tiles (tile kt lives in LDS stage kt % STAGES):
-    //   registers hold every fragment of tile kt; the MFMAs of step ks run while
-    //   the fragments of tile kt+1 step ks-1 are read into the slot step ks-1
-    //   just freed.  Tiles kt+1 .. kt+STAGES are in flight or landed; after the
-    //   barrier of iteration kt the copy of tile kt+STAGES goes into the stage
-    //   tile kt left.
-    const int nk = a.K / BK;
+    // Fragment step ks of a tile: lanes 0-31 take K chunk 2ks, lanes 32-63
+    // chunk 2ks+1, of rows base + (lane & 31).  The swizzle key depends on the
+    // low 4 row bits only, so rows +32i share the lane's base offset.
+    // Chunk 2ks + h of a row sits at byte ((2ks + h) ^ key) * 16 of the row,
+    // i.e. at (slot-0 offset) ^ (ks * 32): one XOR per slot and operand.
+    const int fa0 = swz<CPR>(wm * T::WM + (lane & 31), lane >> 5);
+    const int fb0 = swz<CPR>(wn * T::WN + (lane & 31), lane >> 5);
     bf16x8 ra[T::KS][T::TM], rb[T::KS][T::TN];
-    auto read_frags = [&](const char* As, const char* Bs, int ks) {
-        const int c = ks * 2 + (lane >> 5);
+    // Per-lane bases of the stage being read: fa_s = fa0 + stage * A_BYTES
+    // (the stage term sits above bit 14, so the slot XOR below commutes with it).
+    int fa_s = fa0, fb_s = B_BASE + fb0;
+    auto set_stage = [&](int stage) {
+        fa_s = fa0 + stage * T::A_BYTES;
+        fb_s = B_BASE + fb0 + stage * T::B_BYTES;
+    };
+    auto read_slot = [&](int ks) {                               // fragments of step ks
+        const int fa = fa_s ^ (ks * 32), fb = fb_s ^ (ks * 32);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
-            ra[ks][i] = *reinterpret_cast<const bf16x8*>(As + swz<CPR>(wm * T::WM + i * 32 + (lane & 31), c));
+            ra[ks][i] = *(lds_frag*)((lds_char*)lds + fa + i * 32 * T::ROW);
 #pragma unroll
         for (int j = 0; j < T::TN; ++j)
-            rb[ks][j] = *reinterpret_cast<const bf16x8*>(Bs + swz<CPR>(wn * T::WN + j * 32 + (lane & 31), c));
+            rb[ks][j] = *(lds_frag*)((lds_char*)lds + fb + j * 32 * T::ROW);
     };
     auto mfmas = [&](int ks) {
 #pragma unroll
@@ -220,51 +238,86 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             for (int j = 0; j < T::TN; ++j) acc[i][j] = mfma32x32x16(ra[ks][i], rb[ks][j], acc[i][j]);
     };
     constexpr int NR = T::TM + T::TN, NM = T::TM * T::TN;
+    constexpr int PRE = T::KS / 2;          // fragment steps of a tile run before its barrier
 
+    // Software pipeline over K tiles (tile kt lives in LDS stage kt % STAGES;
+    // registers hold every fragment of the tile being multiplied).  Per tile,
+    // in phases the compiler may not reorder across:
+    //   [steps 0 .. PRE-1 of tile kt ran at the end of the previous tile]
+    //   wait until this wave's copy of tile kt+1 landed (its reads of tile kt
+    //   finished long ago); barrier: tile kt+1 is complete in LDS and the
+    //   stage of tile kt is free;
+    //   step PRE      | copy of tile kt+STAGES into the freed stage
+    //                 | reads of tile kt+1 slots 0 .. PRE-1 (their steps are done)
+    //   step s > PRE  | reads of slot s-1
+    //   step 0 of kt+1 | reads of slot KS-1
+    //   steps 1 .. PRE-1 of kt+1
+    // so every read has at least one phase of MFMAs to land before its use or
+    // the next barrier.  Copies are always issued (clamped to the last tile
+    // past the end of K, into a stage that is never multiplied), which keeps
+    // every wait count a compile-time constant.
+    const int nk = a.K / BK;
 #pragma unroll
-    for (int t = 0; t < STAGES; ++t)
-        if (t < nk) issue(t, t);
-    if (nk >= STAGES) wait_vmcnt<(STAGES - 1) * T::NI>();   // tile 0 landed, later tiles may fly
-    else wait_all_memory();
+    for (int t = 0; t < STAGES; ++t) issue(min(t, nk - 1), t);
+    wait_vmcnt<(STAGES - 1) * T::NI>();     // tile 0 landed, later tiles may fly
     __syncthreads();
+    set_stage(0);
 #pragma unroll
-    for (int ks = 0; ks < T::KS; ++ks) read_frags(smem, smem + T::A_BYTES, ks);
+    for (int ks = 0; ks < T::KS; ++ks) read_slot(ks);
+#pragma unroll
+    for (int ks = 0; ks < PRE; ++ks) mfmas(ks);
+    sched_fence();
 
-    for (int kt = 0; kt < nk; ++kt) {
-        mfmas(0);
-        if (kt + STAGES - 1 < nk) wait_vmcnt<(STAGES - 2) * T::NI>();   // tile kt+1 landed
-        else wait_all_memory();
-        __syncthreads();                    // everyone's tile kt+1 landed; stage of tile kt is free
-        const char* As = smem + ((kt + 1) % STAGES) * T::STAGE;
-        const char* Bs = As + T::A_BYTES;
-        // Step 1 also issues the copy of tile kt+STAGES into the freed stage
-        // (past the end of K the last tile is copied again: the stage is never
-        // read, and the copy keeps the body free of branches so the copies and
-        // fragment reads interleave with the MFMAs).  The last iteration reads
-        // fragments it never uses, likewise harmless in-bounds LDS reads.
+    int st = 0;                             // stage of tile kt
+    for (int kt = 0; kt < nk - 1; ++kt) {
+        const int sn = st + 1 == STAGES ? 0 : st + 1;
+        wait_vmcnt<(STAGES - 2) * T::NI>();                     // own copy of tile kt+1 landed
+        __syncthreads();
+        set_stage(sn);
+        sched_fence();
+        // step PRE | copy of tile kt+STAGES | reads of slots 0 .. PRE-1 of tile kt+1
+        mfmas(PRE);
+        issue(min(kt + STAGES, nk - 1), st);
 #pragma unroll
-        for (int ks = 1; ks < T::KS; ++ks) {
-            mfmas(ks);
-            if (ks == 1) issue(min(kt + STAGES, nk - 1), kt % STAGES);
-            read_frags(As, Bs, ks - 1);
-            if (ks == 1) {
+        for (int q = 0; q < PRE; ++q) read_slot(q);
+        constexpr int NRD = PRE * NR;
 #pragma unroll
-                for (int r = 0; r < T::NI; ++r) {
-                    sched_group<0x008, 1>();
-                    sched_group<0x020, 1>();     // one global->LDS copy
-                    if (r < NR) sched_group<0x100, 1>();
-                }
-                if (NM > T::NI) sched_group<0x008, (NM > T::NI ? NM - T::NI : 1)>();
-            } else {
+        for (int r = 0; r < NM; ++r) {
+            sched_group<0x008, 1>();
 #pragma unroll
-                for (int r = 0; r < NR; ++r) {
-                    sched_group<0x008, (NM / NR > 0 ? NM / NR : 1)>();
-                    sched_group<0x100, 1>();
-                }
-            }
+            for (int c = r * T::NI / NM; c < (r + 1) * T::NI / NM; ++c) sched_group<0x020, 1>();
+#pragma unroll
+            for (int c = r * NRD / NM; c < (r + 1) * NRD / NM; ++c) sched_group<0x100, 1>();
         }
-        read_frags(As, Bs, T::KS - 1);
+        sched_fence();
+#pragma unroll
+        for (int ks = PRE + 1; ks < T::KS; ++ks) {                // step ks | reads of slot ks-1
+            mfmas(ks);
+            read_slot(ks - 1);
+#pragma unroll
+            for (int r = 0; r < NM; ++r) {
+                sched_group<0x008, 1>();
+#pragma unroll
+                for (int c = r * NR / NM; c < (r + 1) * NR / NM; ++c) sched_group<0x100, 1>();
+            }
+            sched_fence();
+        }
+        mfmas(0);                                                 // step 0 of tile kt+1 | last slot
+        read_slot(T::KS - 1);
+#pragma unroll
+        for (int r = 0; r < NM; ++r) {
+            sched_group<0x008, 1>();
+#pragma unroll
+            for (int c = r * NR / NM; c < (r + 1) * NR / NM; ++c) sched_group<0x100, 1>();
+        }
+        sched_fence();
+#pragma unroll
+        for (int ks = 1; ks < PRE; ++ks) mfmas(ks);
+        sched_fence();
+        st = sn;
     }
+#pragma unroll
+    for (int ks = PRE; ks < T::KS; ++ks) mfmas(ks);             // last tile
     wait_all_memory();
     __syncthreads();                        // LDS is reused by the epilogues
 
