@@ -9,7 +9,6 @@
 //         -> final rmsnorm of draft rows -> LM-head GEMM with fused softmax
 //            partials -> merge -> threshold edit.
 #include <math.h>
-#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -404,7 +403,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = a_rows;
         a.out = hexp;
         a.ldo = F;
-        a.variant = getenv("XV") ? atoi(getenv("XV")) : 2;
+        a.variant = 2;
         TRY(gemm(x, "gemm_expert_gate_up", a, EPI_SWIGLU, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     {
@@ -416,7 +415,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = nullptr;
         a.out = y;
         a.ldo = d;
-        a.variant = getenv("XV") ? atoi(getenv("XV")) : 2;
+        a.variant = 2;
         TRY(gemm(x, "gemm_expert_down", a, EPI_BF16, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d, x.st));
