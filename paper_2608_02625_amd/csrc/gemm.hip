@@ -16,6 +16,9 @@
 // Workgroup ids are remapped so that each of the 8 XCDs (which receive
 // workgroups round-robin) processes a contiguous range of tiles; within that
 // range dense GEMMs raster group_m row-tiles at a time to keep operands in L2.
+#include <algorithm>
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -109,48 +112,61 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
 template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void gemm_kernel(GemmArgs a) {
     using T = TileCfg<BM, BN, BK, STAGES, NW>;
-    __shared__ __attribute__((aligned(16))) char smem[T::LDS];
+    // LM-head partial merge buffer, past the K stages (which may already hold
+    // the next tile's copies while this tile's epilogue runs).
+    constexpr int XBUF = EPI == EPI_LMHEAD ? (NW / 2) * T::TN * 32 * 16 : 0;
+    __shared__ __attribute__((aligned(16))) char smem[T::LDS + XBUF];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / (NW / 2), wn = wave % (NW / 2);
     const int tiles_n = (a.N + BN - 1) / BN;
 
-    // ---------------------------------------------------------------- tile decode
+    // ---------------------------------------------------------------- tiles
+    // Persistent: workgroup w runs on XCD w % 8 (workgroups are dealt to the
+    // XCDs round-robin; the grid is a multiple of 8) and walks that XCD's
+    // contiguous share of the tiles with a stride of grid/8, so operands shared
+    // by neighbouring tiles stay in that XCD's L2.
     const int tiles_m_or_listed = GROUPED ? *a.n_tiles : (a.M + BM - 1) / BM;
     const int total = tiles_m_or_listed * tiles_n;
     const int chunk = (total + 7) >> 3;
-    const int w = blockIdx.x;
-    const int local = w >> 3;
-    if (local >= chunk) return;
-    const int L = (w & 7) * chunk + local;
-    if (L >= total) return;
-    int ti, tn;
-    if (GROUPED || a.group_m <= 1) {
-        ti = L / tiles_n;
-        tn = L - ti * tiles_n;
-    } else {
-        const int tiles_m = tiles_m_or_listed;
-        const int per_group = a.group_m * tiles_n;
-        const int grp = L / per_group;
-        const int first_m = grp * a.group_m;
-        const int gsz = min(tiles_m - first_m, a.group_m);
-        const int r = L - grp * per_group;
-        ti = first_m + r % gsz;
-        tn = r / gsz;
-    }
-    int g = 0, m0, row_base = 0, rows;
-    if (GROUPED) {
-        const int2 t = a.tile_tab[ti];
-        g = t.x;
-        m0 = t.y;
-        row_base = a.grp_off[g];
-        rows = a.grp_off[g + 1] - row_base;
-    } else {
-        m0 = ti * BM;
-        rows = a.M;
-    }
-    const int n0 = tn * BN;
-    const bf16_t* Bg = a.B + (GROUPED ? (int64_t)g * a.b_group_stride : 0);
+    const int x_end = min(((int)blockIdx.x & 7) * chunk + chunk, total);
+    const int stride = (int)gridDim.x >> 3;
+    int L = ((int)blockIdx.x & 7) * chunk + ((int)blockIdx.x >> 3);
+    if (L >= x_end) return;
+    struct TileIdx {
+        int g, m0, row_base, rows, n0;
+    };
+    auto decode = [&](int L) {
+        int ti, tn;
+        if (GROUPED || a.group_m <= 1) {
+            ti = L / tiles_n;
+            tn = L - ti * tiles_n;
+        } else {
+            const int tiles_m = tiles_m_or_listed;
+            const int per_group = a.group_m * tiles_n;
+            const int grp = L / per_group;
+            const int first_m = grp * a.group_m;
+            const int gsz = min(tiles_m - first_m, a.group_m);
+            const int r = L - grp * per_group;
+            ti = first_m + r % gsz;
+            tn = r / gsz;
+        }
+        TileIdx t;
+        if (GROUPED) {
+            const int2 e = a.tile_tab[ti];
+            t.g = uniform(e.x);
+            t.m0 = uniform(e.y);
+            t.row_base = uniform(a.grp_off[t.g]);
+            t.rows = uniform(a.grp_off[t.g + 1]) - t.row_base;
+        } else {
+            t.g = 0;
+            t.m0 = ti * BM;
+            t.row_base = 0;
+            t.rows = a.M;
+        }
+        t.n0 = tn * BN;
+        return t;
+    };
 
     // ---------------------------------------------------------------- main loop
     // Operands go global -> LDS directly (buffer_load_dwordx4 ... lds): one
@@ -168,23 +184,26 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const int wv = uniform(wave);
     const int rin = lane / CPR, pc = lane % CPR;
     const bool gather = GROUPED && a.a_rows != nullptr;
-    const bf16_t* a_tile = gather ? a.A : a.A + (int64_t)uniform(row_base + m0) * a.lda;
-    const buf_rsrc_t a_rsrc = make_rsrc(a_tile);
-    const buf_rsrc_t b_rsrc = make_rsrc(Bg + (int64_t)n0 * a.ldb);
+    buf_rsrc_t a_rsrc, b_rsrc;
     uint32_t a_off[T::A_INSTR], b_off[T::B_INSTR];
+    auto setup_copies = [&](const TileIdx& t) {
+        const bf16_t* Bg = a.B + (GROUPED ? (int64_t)t.g * a.b_group_stride : 0);
+        a_rsrc = make_rsrc(gather ? a.A : a.A + (int64_t)(t.row_base + t.m0) * a.lda);
+        b_rsrc = make_rsrc(Bg + (int64_t)t.n0 * a.ldb);
 #pragma unroll
-    for (int p = 0; p < T::A_INSTR; ++p) {
-        const int tr = (wv * T::A_INSTR + p) * RPB + rin;         // row within the tile
-        const int r = min(m0 + tr, rows - 1);
-        const int64_t grow = gather ? (int64_t)a.a_rows[row_base + r] : (int64_t)(r - m0);
-        a_off[p] = (uint32_t)(grow * a.lda * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
-    }
+        for (int p = 0; p < T::A_INSTR; ++p) {
+            const int tr = (wv * T::A_INSTR + p) * RPB + rin;     // row within the tile
+            const int r = min(t.m0 + tr, t.rows - 1);
+            const int64_t grow = gather ? (int64_t)a.a_rows[t.row_base + r] : (int64_t)(r - t.m0);
+            a_off[p] = (uint32_t)(grow * a.lda * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
+        }
 #pragma unroll
-    for (int p = 0; p < T::B_INSTR; ++p) {
-        const int tr = (wv * T::B_INSTR + p) * RPB + rin;
-        const int n = min(n0 + tr, a.N - 1) - n0;
-        b_off[p] = (uint32_t)((int64_t)n * a.ldb * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
-    }
+        for (int p = 0; p < T::B_INSTR; ++p) {
+            const int tr = (wv * T::B_INSTR + p) * RPB + rin;
+            const int n = min(t.n0 + tr, a.N - 1) - t.n0;
+            b_off[p] = (uint32_t)((int64_t)n * a.ldb * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
+        }
+    };
     const lds_ptr_t lds = (lds_ptr_t)smem;
     typedef __attribute__((address_space(3))) char lds_char;
     typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
@@ -200,12 +219,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     };
 
     f32x16 acc[T::TM][T::TN];
-#pragma unroll
-    for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::TN; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
     // Fragment step ks of a tile: lanes 0-31 take K chunk 2ks, lanes 32-63
     // chunk 2ks+1, of rows base + (lane & 31).  The swizzle key depends on the
@@ -257,43 +270,76 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     // past the end of K, into a stage that is never multiplied), which keeps
     // every wait count a compile-time constant.
     const int nk = a.K / BK;
+    TileIdx cur = decode(L);
+    setup_copies(cur);
 #pragma unroll
     for (int t = 0; t < STAGES; ++t) issue(min(t, nk - 1), t);
-    wait_vmcnt<(STAGES - 1) * T::NI>();     // tile 0 landed, later tiles may fly
-    __syncthreads();
-    set_stage(0);
-#pragma unroll
-    for (int ks = 0; ks < T::KS; ++ks) read_slot(ks);
-#pragma unroll
-    for (int ks = 0; ks < PRE; ++ks) mfmas(ks);
-    sched_fence();
 
-    int st = 0;                             // stage of tile kt
-    for (int kt = 0; kt < nk - 1; ++kt) {
-        const int sn = st + 1 == STAGES ? 0 : st + 1;
-        wait_vmcnt<(STAGES - 2) * T::NI>();                     // own copy of tile kt+1 landed
-        __syncthreads();
-        set_stage(sn);
-        sched_fence();
-        // step PRE | copy of tile kt+STAGES | reads of slots 0 .. PRE-1 of tile kt+1
-        mfmas(PRE);
-        issue(min(kt + STAGES, nk - 1), st);
+    // ---------------------------------------------------------------- per tile
+    while (true) {
+    const int m0 = cur.m0, rows = cur.rows, row_base = cur.row_base, n0 = cur.n0;
 #pragma unroll
-        for (int q = 0; q < PRE; ++q) read_slot(q);
-        constexpr int NRD = PRE * NR;
+    for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-        for (int r = 0; r < NM; ++r) {
-            sched_group<0x008, 1>();
+        for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-            for (int c = r * T::NI / NM; c < (r + 1) * T::NI / NM; ++c) sched_group<0x020, 1>();
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    wait_vmcnt<(STAGES - 1) * T::NI>();     // K tile 0 landed, later ones may fly
+    __syncthreads();
+    // In grouped mode the last row tile of a group is often partly empty; a
+    // wave whose rows all lie past the group's end skips its MFMAs (and
+    // fragment reads) but still copies and meets every barrier.
+    auto run = [&](auto active) {
+        constexpr bool ACTIVE = decltype(active)::value;
+        set_stage(0);
+        if constexpr (ACTIVE) {
 #pragma unroll
-            for (int c = r * NRD / NM; c < (r + 1) * NRD / NM; ++c) sched_group<0x100, 1>();
+            for (int ks = 0; ks < T::KS; ++ks) read_slot(ks);
+#pragma unroll
+            for (int ks = 0; ks < PRE; ++ks) mfmas(ks);
         }
         sched_fence();
+
+        int st = 0;                             // stage of tile kt
+        for (int kt = 0; kt < nk - 1; ++kt) {
+            const int sn = st + 1 == STAGES ? 0 : st + 1;
+            wait_vmcnt<(STAGES - 2) * T::NI>();                     // own copy of tile kt+1 landed
+            __syncthreads();
+            set_stage(sn);
+            sched_fence();
+            // step PRE | copy of tile kt+STAGES | reads of slots 0 .. PRE-1 of tile kt+1
+            if constexpr (ACTIVE) mfmas(PRE);
+            issue(min(kt + STAGES, nk - 1), st);
+            if constexpr (!ACTIVE) {
+                st = sn;
+                continue;
+            }
 #pragma unroll
-        for (int ks = PRE + 1; ks < T::KS; ++ks) {                // step ks | reads of slot ks-1
-            mfmas(ks);
-            read_slot(ks - 1);
+            for (int q = 0; q < PRE; ++q) read_slot(q);
+            constexpr int NRD = PRE * NR;
+#pragma unroll
+            for (int r = 0; r < NM; ++r) {
+                sched_group<0x008, 1>();
+#pragma unroll
+                for (int c = r * T::NI / NM; c < (r + 1) * T::NI / NM; ++c) sched_group<0x020, 1>();
+#pragma unroll
+                for (int c = r * NRD / NM; c < (r + 1) * NRD / NM; ++c) sched_group<0x100, 1>();
+            }
+            sched_fence();
+#pragma unroll
+            for (int ks = PRE + 1; ks < T::KS; ++ks) {                // step ks | reads of slot ks-1
+                mfmas(ks);
+                read_slot(ks - 1);
+#pragma unroll
+                for (int r = 0; r < NM; ++r) {
+                    sched_group<0x008, 1>();
+#pragma unroll
+                    for (int c = r * NR / NM; c < (r + 1) * NR / NM; ++c) sched_group<0x100, 1>();
+                }
+                sched_fence();
+            }
+            mfmas(0);                                                 // step 0 of tile kt+1 | last slot
+            read_slot(T::KS - 1);
 #pragma unroll
             for (int r = 0; r < NM; ++r) {
                 sched_group<0x008, 1>();
@@ -301,25 +347,30 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                 for (int c = r * NR / NM; c < (r + 1) * NR / NM; ++c) sched_group<0x100, 1>();
             }
             sched_fence();
+#pragma unroll
+            for (int ks = 1; ks < PRE; ++ks) mfmas(ks);
+            sched_fence();
+            st = sn;
         }
-        mfmas(0);                                                 // step 0 of tile kt+1 | last slot
-        read_slot(T::KS - 1);
+        if constexpr (ACTIVE) {
 #pragma unroll
-        for (int r = 0; r < NM; ++r) {
-            sched_group<0x008, 1>();
-#pragma unroll
-            for (int c = r * NR / NM; c < (r + 1) * NR / NM; ++c) sched_group<0x100, 1>();
+            for (int ks = PRE; ks < T::KS; ++ks) mfmas(ks);         // last tile
         }
-        sched_fence();
-#pragma unroll
-        for (int ks = 1; ks < PRE; ++ks) mfmas(ks);
-        sched_fence();
-        st = sn;
-    }
-#pragma unroll
-    for (int ks = PRE; ks < T::KS; ++ks) mfmas(ks);             // last tile
+    };
+    if (!GROUPED || m0 + wm * T::WM < rows) run(std::true_type());
+    else run(std::false_type());
+    // Every wave is done with this tile's LDS and no copy of it is in flight:
+    // the next tile's first K tiles are copied while this tile's epilogue runs.
     wait_all_memory();
-    __syncthreads();                        // LDS is reused by the epilogues
+    __syncthreads();
+    const int L_next = L + stride;
+    const bool more = L_next < x_end;
+    if (more) {
+        cur = decode(L_next);
+        setup_copies(cur);
+#pragma unroll
+        for (int t = 0; t < STAGES; ++t) issue(min(t, nk - 1), t);
+    }
 
     // ---------------------------------------------------------------- epilogues
     // acc[i][j][e] holds C[row][col] with
@@ -414,7 +465,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
         }
         // Merge the two waves that share these token columns (wm = 0, 1).
-        float4* xbuf = reinterpret_cast<float4*>(smem);
+        float4* xbuf = reinterpret_cast<float4*>(smem + T::LDS);
         if (wm == 1 && lane < 32) {
 #pragma unroll
             for (int j = 0; j < T::TN; ++j)
@@ -435,6 +486,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             }
         }
     }
+    if (!more) break;
+    L = L_next;
+    }
 }
 
 template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
@@ -442,13 +496,25 @@ hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     if constexpr (EPI == EPI_QKV && (BM / 2) % 128 != 0) {
         return hipErrorInvalidValue;                       // RoPE pairs must stay inside one wave
     } else {
+    auto kernel = gemm_kernel<BM, BN, BK, STAGES, NW, EPI, GROUPED>;
+    // Workgroups that fit on the device at once (a multiple of 8, one share
+    // per XCD); a persistent grid of at most that many walks all tiles.
+    static int resident = 0;
+    if (resident == 0) {
+        int dev = 0, cus = 0, occ = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, NW * 64, 0);
+        if (e != hipSuccess) return e;
+        resident = std::max(8, cus * std::max(occ, 1) / 8 * 8);
+    }
     const int tiles_n = (a.N + BN - 1) / BN;
     const int tiles_m = GROUPED ? max_tiles : (a.M + BM - 1) / BM;
     int64_t blocks = (int64_t)tiles_m * tiles_n;
-    blocks = (blocks + 7) / 8 * 8;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, STAGES, NW, EPI, GROUPED>), dim3((unsigned)blocks), dim3(NW * 64), 0, st, a);
+    blocks = std::min<int64_t>((blocks + 7) / 8 * 8, resident);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(NW * 64), 0, st, a);
     return hipGetLastError();
     }
 }
