@@ -6,13 +6,18 @@
 // only masked entries.
 //
 // One workgroup = 4 waves = 128 queries of one (batch, head); each wave owns 32
-// queries.  K tiles [64 keys][hd] and V^T tiles [hd][64 keys] are staged in LDS
-// (two stages, register-prefetched).  Scores are computed transposed,
-// S^T = K Q^T, so that each lane owns one query column: the online-softmax
-// statistics stay lane-local (plus one exchange with lane^32), and the
-// probabilities feed the next MFMA directly from registers as the B operand of
-// O^T = V^T P^T, with the matching key order read from the V^T tile.  V is
-// stored row-major like K and transposed while it is written to LDS.
+// queries.  Per 64-key tile, K [64 keys][hd] and V^T [hd][64 keys] are copied
+// global -> LDS by buffer loads (two stages, XOR-swizzled 16-byte chunks).
+// Scores are computed transposed, S^T = K Q^T, so that each lane owns one
+// query column: the online-softmax statistics stay lane-local (plus one
+// exchange with lane^32) and the probabilities feed the next MFMA straight
+// from registers as the B operand of O^T = V^T P^T.  V^T arrives from the QKV
+// projection with its keys already in the order that operand needs (vt_pos),
+// so every fragment is one 16-byte LDS read.
+// The running maximum is only moved (and the accumulator rescaled) when a
+// tile raises it by more than 2^8 in the exp2 domain; in between,
+// probabilities up to 2^8 are accumulated, which the final division by the
+// running sum cancels exactly.
 #include "common.h"
 #include "kernels.h"
 
@@ -20,25 +25,33 @@ namespace {
 
 template <int HD>
 struct AttnCfg {
-    static constexpr int KEYS = 64;
-    static constexpr int K_STRIDE = HD * 2 + 16;      // bytes per K row in LDS
-    static constexpr int V_STRIDE = KEYS * 2 + 8;     // bytes per V^T row in LDS
-    static constexpr int K_BYTES = KEYS * K_STRIDE;
-    static constexpr int V_BYTES = HD * V_STRIDE;
+    static constexpr int KEYS = 64;                     // keys per tile
+    static constexpr int K_CPR = HD / 8;                // 16-byte chunks per K row
+    static constexpr int K_ROW = HD * 2;
+    static constexpr int K_BYTES = KEYS * K_ROW;
+    static constexpr int V_CPR = KEYS / 8;              // 16-byte chunks per V^T row
+    static constexpr int V_ROW = KEYS * 2;
+    static constexpr int V_BYTES = HD * V_ROW;
     static constexpr int STAGE = K_BYTES + V_BYTES;
-    static constexpr int K_CHUNKS_ROW = HD / 8;       // 16-byte chunks per K row
-    static constexpr int K_PASSES = KEYS * K_CHUNKS_ROW / 256;
-    static constexpr int V_PASSES = HD / 8 / 4;       // 16-byte V chunks per lane (lane = key)
-    static constexpr int NB = HD / 32;                // 32-row blocks of O^T
-    static constexpr int NKS = HD / 16;               // K16 steps over hd
+    static constexpr int K_INSTR = K_BYTES / 1024 / 4;  // 1 KB copies per wave per tile
+    static constexpr int V_INSTR = V_BYTES / 1024 / 4;
+    static constexpr int NB = HD / 32;                  // 32-row blocks of O^T
+    static constexpr int NKS = HD / 16;                 // K16 steps over hd
 };
 
+// XOR key of the 16-byte chunks of an LDS row of CPR chunks; fragment reads of
+// 32 consecutive rows at one logical chunk then hit distinct banks.
+template <int CPR>
+__device__ __forceinline__ int chunk_key(int row) {
+    if constexpr (CPR == 16) return row & 15;
+    else return (row & 7) ^ ((row >> 3) & 1);
+}
+
 template <int HD>
-__global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
-                                                   const bf16_t* __restrict__ K,
-                                                   const bf16_t* __restrict__ V,
-                                                   bf16_t* __restrict__ O, int S, int H,
-                                                   int KV, float scale_log2) {
+__global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
+                                                   const bf16_t* Vt, bf16_t* __restrict__ O, int S,
+                                                   int H, int KV, float scale_log2, uint32_t k_bytes,
+                                                   uint32_t v_bytes) {
     using C = AttnCfg<HD>;
     __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
 
@@ -47,10 +60,51 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
     const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int kvh = h / (H / KV);
     const int q = qb * 128 + wave * 32 + j;
+    const int VS = vt_stride(S);
+    const int wv = uniform(wave);
 
     const bf16_t* Qh = Q + ((int64_t)b * H + h) * S * HD;
-    const bf16_t* Kh = K + ((int64_t)b * KV + kvh) * S * HD;
-    const bf16_t* Vh = V + ((int64_t)b * KV + kvh) * S * HD;
+    // The last K tile reads up to 63 rows past S: rows of the next head
+    // (masked), or past the last head into the buffer's one-tile tail.  V^T
+    // rows are padded to whole tiles, so V^T reads stay inside their row.
+    const buf_rsrc_t k_rsrc = make_rsrc(K, (int)k_bytes);
+    const buf_rsrc_t v_rsrc = make_rsrc(Vt, (int)v_bytes);
+    const uint32_t k_base = (uint32_t)(((int64_t)b * KV + kvh) * S * HD * 2);
+    const uint32_t v_base = (uint32_t)(((int64_t)b * KV + kvh) * HD * VS * 2);
+
+    // Per-lane byte offsets of this wave's copies (tile-relative; the key
+    // offset of the tile goes into the scalar offset).
+    uint32_t k_off[C::K_INSTR], v_off[C::V_INSTR];
+    {
+        constexpr int KRB = 64 / C::K_CPR;              // K rows per 1 KB block
+#pragma unroll
+        for (int p = 0; p < C::K_INSTR; ++p) {
+            const int row = (wv * C::K_INSTR + p) * KRB + lane / C::K_CPR;
+            const int pc = lane % C::K_CPR;
+            k_off[p] = k_base + (uint32_t)(row * HD * 2 + ((pc ^ chunk_key<C::K_CPR>(row)) * 16));
+        }
+        constexpr int VRB = 64 / C::V_CPR;              // V^T rows per 1 KB block
+#pragma unroll
+        for (int p = 0; p < C::V_INSTR; ++p) {
+            const int row = (wv * C::V_INSTR + p) * VRB + lane / C::V_CPR;
+            const int pc = lane % C::V_CPR;
+            v_off[p] = v_base + (uint32_t)(row * VS * 2 + ((pc ^ chunk_key<C::V_CPR>(row)) * 16));
+        }
+    }
+    const lds_ptr_t lds = (lds_ptr_t)smem;
+    typedef __attribute__((address_space(3))) char lds_char;
+    typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
+    auto issue = [&](int kt, int stage) {
+        const int k_soff = kt * C::KEYS * HD * 2, v_soff = kt * C::KEYS * 2;
+        const int kd = stage * C::STAGE + wv * C::K_INSTR * 1024;
+        const int vd = stage * C::STAGE + C::K_BYTES + wv * C::V_INSTR * 1024;
+#pragma unroll
+        for (int p = 0; p < C::K_INSTR; ++p)
+            lds_dma16_buf(k_rsrc, k_off[p], k_soff, (lds_ptr_t)((lds_char*)lds + kd + p * 1024));
+#pragma unroll
+        for (int p = 0; p < C::V_INSTR; ++p)
+            lds_dma16_buf(v_rsrc, v_off[p], v_soff, (lds_ptr_t)((lds_char*)lds + vd + p * 1024));
+    };
 
     bf16x8 qf[C::NKS];
     {
@@ -64,53 +118,22 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
     for (int n = 0; n < C::NB; ++n)
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[n][e] = 0.f;
-    float m_run = -INFINITY, l_run = 0.f;
+    float m_run = -INFINITY, l_run = 0.f;           // m_run in raw score units
 
-    // staging registers
-    u32x4 rk[C::K_PASSES], rv[C::V_PASSES];
-    const int kc = tid % C::K_CHUNKS_ROW, kr = tid / C::K_CHUNKS_ROW;
-    constexpr int K_ROWS_PER_PASS = 256 / C::K_CHUNKS_ROW;
-
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int p = 0; p < C::K_PASSES; ++p) {
-            const int key = k0 + kr + p * K_ROWS_PER_PASS;
-            u32x4 v = *reinterpret_cast<const u32x4*>(Kh + (int64_t)min(key, S - 1) * HD + kc * 8);
-            if (key >= S) v = u32x4{0u, 0u, 0u, 0u};
-            rk[p] = v;
-        }
-#pragma unroll
-        for (int p = 0; p < C::V_PASSES; ++p) {
-            const int key = k0 + lane;
-            const int chunk = wave + 4 * p;
-            u32x4 v = *reinterpret_cast<const u32x4*>(Vh + (int64_t)min(key, S - 1) * HD + chunk * 8);
-            if (key >= S) v = u32x4{0u, 0u, 0u, 0u};
-            rv[p] = v;
-        }
-    };
-    auto lstore = [&](int buf) {
-        char* Ks = smem + buf * C::STAGE;
-        char* Vs = Ks + C::K_BYTES;
-#pragma unroll
-        for (int p = 0; p < C::K_PASSES; ++p)
-            *reinterpret_cast<u32x4*>(Ks + (kr + p * K_ROWS_PER_PASS) * C::K_STRIDE + kc * 16) = rk[p];
-#pragma unroll
-        for (int p = 0; p < C::V_PASSES; ++p) {
-            char* dst = Vs + (wave + 4 * p) * 8 * C::V_STRIDE + lane * 2;
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                *reinterpret_cast<bf16_t*>(dst + i * C::V_STRIDE) = (bf16_t)(rv[p][i >> 1] >> (16 * (i & 1)));
-        }
-    };
+    // Fragment bases: K row c*32 + j, chunk 2ks + g; V^T row n*32 + j,
+    // chunk 4c + 2s2 + g.  The XOR key depends on the low row bits only.
+    const int kfrag = j * C::K_ROW;
+    const int kkey = chunk_key<C::K_CPR>(j);
+    const int vfrag = C::K_BYTES + j * C::V_ROW;
+    const int vkey = chunk_key<C::V_CPR>(j);
 
     const int nkt = (S + C::KEYS - 1) / C::KEYS;
-    gload(0);
-    lstore(0);
-    __syncthreads();
+    issue(0, 0);
     for (int kt = 0; kt < nkt; ++kt) {
-        if (kt + 1 < nkt) gload((kt + 1) * C::KEYS);
-        const char* Ks = smem + (kt & 1) * C::STAGE;
-        const char* Vs = Ks + C::K_BYTES;
+        wait_all_memory();                          // this wave's copies of tile kt landed
+        __syncthreads();                            // everyone's; stage of tile kt-1 is free
+        if (kt + 1 < nkt) issue(kt + 1, (kt + 1) & 1);
+        const int sb = (kt & 1) * C::STAGE;
         const int k0 = kt * C::KEYS;
 
         // S^T for 64 keys (two 32-key chunks): lane holds query j, keys
@@ -120,64 +143,63 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
         for (int c = 0; c < 2; ++c) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) st[c][e] = 0.f;
-            const char* krow = Ks + (c * 32 + j) * C::K_STRIDE + g * 16;
 #pragma unroll
             for (int ks = 0; ks < C::NKS; ++ks) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + ks * 32);
+                const int off = sb + c * 32 * C::K_ROW + kfrag + (((2 * ks + g) ^ kkey) << 4);
+                const bf16x8 kf = *(lds_frag*)((lds_char*)lds + off);
                 st[c] = mfma32x32x16(kf, qf[ks], st[c]);
             }
+        }
+        if (k0 + C::KEYS > S) {                     // last tile: keys past S do not exist
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    if (k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= S) st[c][e] = -INFINITY;
         }
         float mt = -INFINITY;
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int key = k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
-                const float s = (key < S) ? st[c][e] * scale_log2 : -INFINITY;
-                st[c][e] = s;
-                mt = fmaxf(mt, s);
-            }
+            for (int e = 0; e < 16; ++e) mt = fmaxf(mt, st[c][e]);
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float m_new = fmaxf(m_run, mt);
-        const float alpha = exp2f(m_run - m_new);
+        if (__any((mt - m_run) * scale_log2 > 8.f)) {
+            const float m_new = fmaxf(m_run, mt);
+            const float alpha = exp2f((m_run - m_new) * scale_log2);
+            l_run *= alpha;
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) oacc[n][e] *= alpha;
+            m_run = m_new;
+        }
+        const float nb = -m_run * scale_log2;
         float lt = 0.f;
         bf16x8 pf[2][2];
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const float p = exp2f(st[c][e] - m_new);
+                const float p = exp2f(fmaf(st[c][e], scale_log2, nb));
                 lt += p;
                 pf[c][e >> 3][e & 7] = (__bf16)p;
             }
-        lt += __shfl_xor(lt, 32, 64);
-        l_run = l_run * alpha + lt;
-        m_run = m_new;
+        l_run += lt;
+
+        // O^T += V^T P^T: one 16-byte V^T read per fragment
 #pragma unroll
         for (int n = 0; n < C::NB; ++n)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) oacc[n][e] *= alpha;
-
-        // O^T += V^T P^T
-#pragma unroll
-        for (int n = 0; n < C::NB; ++n) {
-            const char* vrow = Vs + (n * 32 + j) * C::V_STRIDE;
 #pragma unroll
             for (int c = 0; c < 2; ++c)
 #pragma unroll
                 for (int s2 = 0; s2 < 2; ++s2) {
-                    const int key = c * 32 + 16 * s2 + 4 * g;
-                    const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + key * 2);
-                    const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + (key + 8) * 2);
-                    u32x4 w4 = u32x4{lo[0], lo[1], hi[0], hi[1]};
-                    const bf16x8 vf = __builtin_bit_cast(bf16x8, w4);
+                    const int off = sb + vfrag + n * 32 * C::V_ROW + (((4 * c + 2 * s2 + g) ^ vkey) << 4);
+                    const bf16x8 vf = *(lds_frag*)((lds_char*)lds + off);
                     oacc[n] = mfma32x32x16(vf, pf[c][s2], oacc[n]);
                 }
-        }
-        if (kt + 1 < nkt) lstore((kt + 1) & 1);
-        __syncthreads();
     }
 
+    l_run += __shfl_xor(l_run, 32, 64);
     if (q < S) {
         const float inv = 1.f / l_run;
         bf16_t* orow = O + ((int64_t)b * S + q) * ((int64_t)H * HD) + (int64_t)h * HD;
@@ -195,14 +217,19 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
 
 }  // namespace
 
-hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* v, bf16_t* o, int B,
+hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, bf16_t* o, int B,
                             int S, int H, int KV, int hd, hipStream_t st) {
     const dim3 grid((S + 127) / 128, H, B);
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+    // byte sizes of the K buffer (with its one-tile tail) and of V^T
+    const int64_t kb = ((int64_t)B * KV * S + 64) * hd * 2, vb = (int64_t)B * KV * hd * vt_stride(S) * 2;
+    if (kb >= 0x7fffffff || vb >= 0x7fffffff) return hipErrorInvalidValue;   // 32-bit buffer offsets
     if (hd == 128)
-        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, v, o, S, H, KV, scale_log2);
+        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, S, H, KV, scale_log2,
+                           (uint32_t)kb, (uint32_t)vb);
     else if (hd == 64)
-        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, v, o, S, H, KV, scale_log2);
+        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, S, H, KV, scale_log2,
+                           (uint32_t)kb, (uint32_t)vb);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

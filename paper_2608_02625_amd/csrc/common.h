@@ -49,9 +49,9 @@ struct buf_rsrc_t {
     uint32_t w[4];
 };
 #endif
-__device__ __forceinline__ buf_rsrc_t make_rsrc(const void* base) {
+__device__ __forceinline__ buf_rsrc_t make_rsrc(const void* base, int bytes = 0x7fffffff) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 #else
     return buf_rsrc_t{};
 #endif

@@ -179,6 +179,14 @@ __global__ void zero_i32_kernel(int32_t* __restrict__ p, int n) {
     if (i < n) p[i] = 0;
 }
 
+
+__global__ void vt_pad_zero_kernel(bf16_t* vt, int64_t n, int S, int pad, int stride) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int64_t r = i / pad;
+    vt[r * stride + vt_pos(S + (int)(i - r * pad))] = 0;
+}
+
 }  // namespace
 
 void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
@@ -233,4 +241,11 @@ void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int m
 
 void launch_zero_i32(int32_t* p, int n, hipStream_t st) {
     hipLaunchKernelGGL(zero_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
+}
+
+void launch_vt_pad_zero(bf16_t* vt, int64_t rows, int S, hipStream_t st) {
+    const int stride = vt_stride(S), pad = stride - S;
+    const int64_t n = rows * pad;
+    if (n == 0) return;
+    hipLaunchKernelGGL(vt_pad_zero_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, vt, n, S, pad, stride);
 }

@@ -181,8 +181,8 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
     w.x = add(T * d * 4);
     w.h = add(T * d * 2);
     w.q = add((int64_t)B * c.n_heads * S * hd * 2);
-    w.k = add((int64_t)B * c.n_kv_heads * S * hd * 2);
-    w.v = add((int64_t)B * c.n_kv_heads * S * hd * 2);
+    w.k = add(((int64_t)B * c.n_kv_heads * S + 64) * hd * 2);         // + one 64-key tile of tail
+    w.v = add((int64_t)B * c.n_kv_heads * hd * vt_stride((int)S) * 2);   // V^T, rows padded to tiles
     w.attn = add(T * c.n_heads * hd * 2);
     w.rope = add(S * (hd / 2) * 8);
     if (c.n_experts == 0) {
@@ -425,6 +425,7 @@ dlm_status run_layer(Ctx& x, int l) {
 dlm_status run_prologue(Ctx& x, const int32_t* tokens) {
     const dlm_config& c = x.c;
     LAUNCH(x, "rope_table", launch_rope_table(x.at<float2>(x.w.rope), x.S, c.head_dim / 2, (double)c.rope_theta, x.st));
+    LAUNCH(x, "vt_pad_zero", launch_vt_pad_zero(x.at<bf16_t>(x.w.v), (int64_t)x.B * c.n_kv_heads * c.head_dim, x.S, x.st));
     if (tokens) LAUNCH(x, "embed", launch_embed(tokens, x.wt(x.m->plan.emb), x.at<float>(x.w.x), x.T, c.d_model, c.vocab, x.st));
     return DLM_OK;
 }

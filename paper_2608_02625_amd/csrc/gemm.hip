@@ -58,7 +58,8 @@ __device__ __forceinline__ int swz(int row, int chunk) {
 
 // QKV projection, computed transposed: rows = q/k/v features, columns =
 // tokens.  A lane then holds, per accumulator, 4 consecutive features of one
-// token (8-byte stores into Q [B][H][S][hd], K and V [B][KV][S][hd]), and a
+// token (8-byte stores into Q [B][H][S][hd] and K [B][KV][S][hd]; V goes to the
+// transposed layout V^T of kernels.h, consecutive lanes = consecutive keys), and a
 // wave's 128 rows cover whole heads, so the RoPE partners (i, i + hd/2) are in
 // the same lane, accumulator rows i and i + hd/64 (rotate-half, applied in
 // fp32 before rounding).
@@ -101,8 +102,13 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
                     else
                         dst = a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * S + s) * HD + hi0;
                 } else {
+                    // V^T: 4 rows (features) of one key column
                     const int fv = f0 - Hq - Hk;
-                    dst = a.v + (((int64_t)b * a.n_kv + fv / HD) * S + s) * HD + (fv % HD);
+                    const int vs = vt_stride(S);
+                    bf16_t* col = a.v + ((int64_t)(b * a.n_kv + fv / HD) * HD + fv % HD) * vs + vt_pos(s);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) col[(int64_t)r * vs] = f32_to_bf16(v[r]);
+                    continue;
                 }
                 *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
             }

@@ -12,13 +12,21 @@ void launch_init_weights(bf16_t* dst, uint64_t n_phys, uint32_t cols, uint32_t t
 void launch_fill_bf16(bf16_t* dst, uint64_t n, bf16_t v, hipStream_t st);
 void launch_rope_table(float2* tab, int S, int half, double theta, hipStream_t st);
 
+// V is kept transposed for attention: V^T [B][KV][hd][S64], S64 = S rounded up
+// to the 64-key attention tile.  Inside each aligned group of 16 keys the keys
+// are stored in the order an MFMA fragment consumes them: position of key s =
+// s with bits 2 and 3 exchanged (keys 4-7 and 8-11 of the group trade
+// places).  Positions of keys >= S are zero.
+__host__ __device__ inline int vt_pos(int s) { return (s & ~12) | ((s & 4) << 1) | ((s & 8) >> 1); }
+__host__ __device__ inline int vt_stride(int S) { return (S + 63) & ~63; }
+
 // ----------------------------------------------------------------- gemm.hip
 enum GemmEpilogue {
     EPI_BF16 = 0,     // out_bf16[row][col]
     EPI_F32 = 1,      // out_f32[row][col]
     EPI_RESID = 2,    // resid_f32[row][col] += acc
     EPI_SWIGLU = 3,   // out_bf16[row][f] = silu(gate) * up, gate/up interleaved in 32-col blocks
-    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K and V [B][KV][S][hd]
+    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K [B][KV][S][hd], V^T (vt_pos)
     EPI_LMHEAD = 5,   // rows = vocab, cols = tokens: per-(vocab tile, token) softmax partials
     EPI_F32_T = 6,    // out_f32[col][row] (transposed store)
 };
@@ -81,6 +89,8 @@ void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, 
 void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int mask_id,
                         int32_t* counter, hipStream_t st);
 void launch_zero_i32(int32_t* p, int n, hipStream_t st);
+// Zero the V^T positions of keys S .. S64-1 in every one of `rows` rows.
+void launch_vt_pad_zero(bf16_t* vt, int64_t rows, int S, hipStream_t st);
 
 // ----------------------------------------------------------------- moe.hip
 // Router softmax + top-k (ties -> lower id) + renormalisation.
