@@ -48,7 +48,7 @@ __device__ __forceinline__ int chunk_key(int row) {
 }
 
 template <int HD>
-__global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
                                                    const bf16_t* Vt, bf16_t* __restrict__ O, int S,
                                                    int H, int KV, float scale_log2, uint32_t k_bytes,
                                                    uint32_t v_bytes) {
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
         if (__any((mt - m_run) * scale_log2 > 8.f)) {
             const float m_new = fmaxf(m_run, mt);
-            const float alpha = exp2f((m_run - m_new) * scale_log2);
+            const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2);
             l_run *= alpha;
 #pragma unroll
             for (int n = 0; n < C::NB; ++n)
@@ -179,10 +179,16 @@ __global__ __launch_bounds__(256) void attn_kernel(const bf16_t* __restrict__ Q,
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const float p = exp2f(fmaf(st[c][e], scale_log2, nb));
-                lt += p;
-                pf[c][e >> 3][e & 7] = (__bf16)p;
+            for (int s2 = 0; s2 < 2; ++s2) {
+                u32x4 w;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(st[c][8 * s2 + 2 * t], scale_log2, nb));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(st[c][8 * s2 + 2 * t + 1], scale_log2, nb));
+                    lt += p0 + p1;
+                    w[t] = pack_bf16x2(p0, p1);
+                }
+                pf[c][s2] = __builtin_bit_cast(bf16x8, w);
             }
         l_run += lt;
 

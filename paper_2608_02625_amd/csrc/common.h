@@ -17,16 +17,29 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
     return __uint_as_float(((uint32_t)h) << 16);
 }
 
-// Round-to-nearest-even float -> bfloat16 (finite inputs; NaN stays NaN).
+// float -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950; NaN
+// stays NaN).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_bit_cast(bf16_t, (__bf16)f);
+#else
     uint32_t u = __float_as_uint(f);
     if ((u & 0x7f800000u) == 0x7f800000u) return (bf16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
     u += 0x7fffu + ((u >> 16) & 1u);
     return (bf16_t)(u >> 16);
+#endif
 }
 
+// Two floats -> packed bf16 pair (lo in bits 0-15), one conversion instruction.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+#else
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+#endif
 }
 
 // gfx950 intrinsics used by the kernels.  Their bodies exist only in the
