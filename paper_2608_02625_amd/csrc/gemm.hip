@@ -69,49 +69,66 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
     constexpr int HALF = HD / 2, SPH = HD / 32, POFF = HD / 64;
     const int Hq = a.n_heads * HD, Hk = a.n_kv * HD;
     const int S = a.seq;
+    // A wave's 128 rows start on a head boundary, and the Q/K/V boundaries are
+    // head boundaries: the wave is wholly inside Q, K or V (or past M).
+    const int wrow = m0 + (lrow0 & ~127);
+    if (wrow >= a.M) return;
+    const bool rotate = wrow < Hq + Hk;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int t = n0 + lcol0 + j * 32;                    // token
         if (t >= a.N) continue;
         const int b = t / S, s = t - b * S;
+        if (rotate) {
+            // (cos, sin) of the lane's 4 consecutive pairs for each first-half
+            // 32-row block and each group q, all loaded before use.
+            float4 cs[POFF][4][2];
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+            for (int ih = 0; ih < POFF; ++ih)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int f0 = m0 + lrow0 + i * 32 + 8 * q;       // first of 4 consecutive features
-                if (f0 >= a.M) continue;                           // M is a multiple of HD
-                float v[4];
+                for (int q = 0; q < 4; ++q) {
+                    const int r0 = (lrow0 & 127) + ih * 32 + 8 * q;       // row within the head pair block
+                    const float4* p = reinterpret_cast<const float4*>(a.rope + s * HALF + (r0 % HALF));
+                    cs[ih][q][0] = p[0];
+                    cs[ih][q][1] = p[1];
+                }
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-                bf16_t* dst;
-                if (f0 < Hq + Hk) {
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int f0 = m0 + lrow0 + i * 32 + 8 * q;       // first of 4 consecutive features
                     const int hi0 = f0 % HD;
-                    const float4* cs = reinterpret_cast<const float4*>(a.rope + s * HALF + (hi0 % HALF));
-                    const float4 c01 = cs[0], c23 = cs[1];          // (cos, sin) of 4 consecutive pairs
+                    const int ih = (i % SPH) % POFF;
+                    const float4 c01 = cs[ih][q][0], c23 = cs[ih][q][1];
                     const float cz[4] = {c01.x, c01.z, c23.x, c23.z};
                     const float sn[4] = {c01.y, c01.w, c23.y, c23.w};
+                    float v[4];
                     if ((i % SPH) < POFF) {
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cz[r] - acc[(i + POFF) % TM][j][4 * q + r] * sn[r];
+                        for (int r = 0; r < 4; ++r)
+                            v[r] = acc[i][j][4 * q + r] * cz[r] - acc[(i + POFF) % TM][j][4 * q + r] * sn[r];
                     } else {
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cz[r] + acc[(i + TM - POFF) % TM][j][4 * q + r] * sn[r];
+                        for (int r = 0; r < 4; ++r)
+                            v[r] = acc[i][j][4 * q + r] * cz[r] + acc[(i + TM - POFF) % TM][j][4 * q + r] * sn[r];
                     }
-                    if (f0 < Hq)
-                        dst = a.q + (((int64_t)b * a.n_heads + f0 / HD) * S + s) * HD + hi0;
-                    else
-                        dst = a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * S + s) * HD + hi0;
-                } else {
-                    // V^T: 4 rows (features) of one key column
-                    const int fv = f0 - Hq - Hk;
-                    const int vs = vt_stride(S);
+                    bf16_t* dst = f0 < Hq ? a.q + (((int64_t)b * a.n_heads + f0 / HD) * S + s) * HD + hi0
+                                          : a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * S + s) * HD + hi0;
+                    *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                }
+        } else {
+            // V^T: per accumulator 4 rows (features) of one key column
+            const int vs = vt_stride(S);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int fv = m0 + lrow0 + i * 32 + 8 * q - Hq - Hk;
                     bf16_t* col = a.v + ((int64_t)(b * a.n_kv + fv / HD) * HD + fv % HD) * vs + vt_pos(s);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) col[(int64_t)r * vs] = f32_to_bf16(v[r]);
-                    continue;
+                    for (int r = 0; r < 4; ++r) col[(int64_t)r * vs] = f32_to_bf16(acc[i][j][4 * q + r]);
                 }
-                *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-            }
+        }
     }
 }
 
@@ -384,7 +401,45 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const int lrow0 = wm * T::WM + 4 * (lane >> 5);
     const int lcol0 = wn * T::WN + (lane & 31);
 
-    if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_F32_T) {
+    const bool full_tile = m0 + BM <= rows && n0 + BN <= a.N;
+    if constexpr (EPI == EPI_RESID) {
+        // out[row][col] += acc: per 32-row block all 16 x TN loads are issued
+        // before the adds and stores.
+        float* out = reinterpret_cast<float*>(a.out);
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i) {
+            float old[16][T::TN];
+            const int rb = m0 + lrow0 + i * 32;
+            if (full_tile) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+#pragma unroll
+                    for (int j = 0; j < T::TN; ++j)
+                        old[e][j] = out[(int64_t)(rb + 8 * (e >> 2) + (e & 3)) * a.ldo + n0 + lcol0 + j * 32];
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+#pragma unroll
+                    for (int j = 0; j < T::TN; ++j)
+                        out[(int64_t)(rb + 8 * (e >> 2) + (e & 3)) * a.ldo + n0 + lcol0 + j * 32] =
+                            old[e][j] + acc[i][j][e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+#pragma unroll
+                    for (int j = 0; j < T::TN; ++j) {
+                        const int r = rb + 8 * (e >> 2) + (e & 3), c = n0 + lcol0 + j * 32;
+                        old[e][j] = (r < rows && c < a.N) ? out[(int64_t)r * a.ldo + c] : 0.f;
+                    }
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+#pragma unroll
+                    for (int j = 0; j < T::TN; ++j) {
+                        const int r = rb + 8 * (e >> 2) + (e & 3), c = n0 + lcol0 + j * 32;
+                        if (r < rows && c < a.N) out[(int64_t)r * a.ldo + c] = old[e][j] + acc[i][j][e];
+                    }
+            }
+        }
+    } else if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_T) {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
 #pragma unroll
@@ -401,10 +456,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                         reinterpret_cast<bf16_t*>(a.out)[orow * a.ldo + c] = f32_to_bf16(v);
                     else if constexpr (EPI == EPI_F32)
                         reinterpret_cast<float*>(a.out)[orow * a.ldo + c] = v;
-                    else if constexpr (EPI == EPI_F32_T)
-                        reinterpret_cast<float*>(a.out)[(int64_t)c * a.ldo + orow] = v;
                     else
-                        reinterpret_cast<float*>(a.out)[orow * a.ldo + c] += v;
+                        reinterpret_cast<float*>(a.out)[(int64_t)c * a.ldo + orow] = v;
                 }
             }
     } else if constexpr (EPI == EPI_SWIGLU) {
