@@ -55,13 +55,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     using C = AttnCfg<HD>;
     __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);   // scalar: wave-level branches stay branches
     const int g = lane >> 5, j = lane & 31;
     const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int kvh = h / (H / KV);
     const int q = qb * 128 + wave * 32 + j;
     const int VS = vt_stride(S);
-    const int wv = uniform(wave);
+    const int wv = wave;
 
     const bf16_t* Qh = Q + ((int64_t)b * H + h) * S * HD;
     // The last K tile reads up to 63 rows past S: rows of the next head

@@ -161,8 +161,8 @@ WeightPlan plan_weights(const dlm_config& c) {
 // Workspace carve-up for one (B, P, D).
 struct Workspace {
     size_t total = 0;
-    size_t x, h, q, k, v, attn, rope, hf, logits, ids, wts, grp_off, tile_tab,
-        n_tiles, slot, a_rows, hexp, y, hfin, partials, top1, conf, maxlogit, counters, tokens;
+    size_t x, h, q, k, v, attn, rope, hf, ids, wts, grp_off, tile_tab,
+        n_tiles, slot, a_rows, ecount, hexp, y, hfin, partials, top1, conf, maxlogit, counters, tokens;
     int rows_total = 0, max_tiles = 0, n_vtiles = 0;
 };
 
@@ -191,7 +191,6 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
         const int E = c.n_experts, k = c.top_k, G = E + c.n_shared_experts;
         w.rows_total = (int)(T * k + T * c.n_shared_experts);
         w.max_tiles = (w.rows_total + kExpertBM - 1) / kExpertBM + G;
-        w.logits = add(T * E * 4);
         w.ids = add(T * k * 4);
         w.wts = add(T * k * 4);
         w.grp_off = add((G + 1) * 4);
@@ -199,6 +198,7 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
         w.n_tiles = add(4);
         w.slot = add(T * k * 4);
         w.a_rows = add((int64_t)w.rows_total * 4);
+        w.ecount = add((T + 31) / 32 * E * 4);           // per router workgroup and expert counts
         w.hexp = add((int64_t)w.rows_total * c.expert_ffn_dim * 2);
         w.y = add((int64_t)w.rows_total * d * 2);
     }
@@ -375,7 +375,6 @@ dlm_status run_layer(Ctx& x, int l) {
         return DLM_OK;
     }
     const int E = c.n_experts, kk = c.top_k, NS = c.n_shared_experts, F = c.expert_ffn_dim;
-    float* logits = x.at<float>(x.w.logits);
     int32_t* ids = x.at<int32_t>(x.w.ids);
     float* wts = x.at<float>(x.w.wts);
     int32_t* grp_off = x.at<int32_t>(x.w.grp_off);
@@ -383,17 +382,20 @@ dlm_status run_layer(Ctx& x, int l) {
     int32_t* n_tiles = x.at<int32_t>(x.w.n_tiles);
     int32_t* slot = x.at<int32_t>(x.w.slot);
     int32_t* a_rows = x.at<int32_t>(x.w.a_rows);
+    int32_t* wg_counts = x.at<int32_t>(x.w.ecount);
     bf16_t* hexp = x.at<bf16_t>(x.w.hexp);
     bf16_t* y = x.at<bf16_t>(x.w.y);
     {
-        GemmArgs a = gemm_args(h, d, x.wt(L.wr), d, x.T, E, d);
-        a.out = logits;
-        a.ldo = E;
-        TRY(gemm(x, "gemm_router", a, EPI_F32, false, 128, 64, 0));
+        prof_begin(x, "router_topk");
+        hipError_t e = launch_router_topk(h, x.wt(L.wr), x.T, d, E, kk, ids, wts, slot, wg_counts, x.st);
+        prof_end(x, "router_topk");
+        if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("router_topk: ") + hipGetErrorString(e));
+        prof_begin(x, "dispatch");
+        e = launch_dispatch(ids, x.T, kk, E, NS, kExpertBM, wg_counts, grp_off, tile_tab, n_tiles, slot, a_rows,
+                            x.st);
+        prof_end(x, "dispatch");
+        if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("dispatch: ") + hipGetErrorString(e));
     }
-    LAUNCH(x, "topk", launch_topk(logits, x.T, E, kk, ids, wts, x.st));
-    LAUNCH(x, "dispatch", launch_dispatch(ids, x.T, kk, E, NS, kExpertBM, grp_off, tile_tab, n_tiles, slot,
-                                          a_rows, x.st));
     {
         GemmArgs a = gemm_args(h, d, x.wt(L.wgu), d, 0, 2 * F, d);
         a.b_group_stride = (int64_t)2 * F * d;

@@ -140,7 +140,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     constexpr int XBUF = EPI == EPI_LMHEAD ? (NW / 2) * T::TN * 32 * 16 : 0;
     __shared__ __attribute__((aligned(16))) char smem[T::LDS + XBUF];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);   // scalar: wave-level branches stay branches
     const int wm = wave / (NW / 2), wn = wave % (NW / 2);
     const int tiles_n = (a.N + BN - 1) / BN;
 
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     constexpr int CPR = T::CPR;
     constexpr int RPB = 64 / CPR;                               // tile rows per 1 KB block
     constexpr int B_BASE = STAGES * T::A_BYTES;
-    const int wv = uniform(wave);
+    const int wv = wave;
     const int rin = lane / CPR, pc = lane % CPR;
     const bool gather = GROUPED && a.a_rows != nullptr;
     buf_rsrc_t a_rsrc, b_rsrc;

@@ -93,12 +93,19 @@ void launch_zero_i32(int32_t* p, int n, hipStream_t st);
 void launch_vt_pad_zero(bf16_t* vt, int64_t rows, int S, hipStream_t st);
 
 // ----------------------------------------------------------------- moe.hip
-// Router softmax + top-k (ties -> lower id) + renormalisation.
-void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w, hipStream_t st);
+// Router logits of T tokens (h [T][d] bf16, Wr [E][d] bf16, E <= 256), softmax
+// top-k (k <= 8; ties -> lower id) with renormalised weights.  Tokens are
+// handled 32 per router workgroup: pos[t][j] = rank of the selection among its
+// workgroup's selections of expert ids[t][j]; wg_counts[E][ceil(T/32)] = per
+// expert and workgroup selection counts.
+hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, int E, int k, int32_t* ids,
+                              float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st);
 // Group row ranges (E routed + n_shared groups of T rows), tile table of the
-// grouped GEMM (tile height bm), slot[t][j] and a_rows[row] = token.
-void launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared, int bm, int32_t* grp_off,
-                     int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows, hipStream_t st);
+// grouped GEMM (tile height bm), slot[t][j] (from pos, in place) and
+// a_rows[row] = token.  wg_counts is turned into per-workgroup offsets.
+hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared, int bm, int32_t* wg_counts,
+                           int32_t* grp_off, int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows,
+                           hipStream_t st);
 // x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[shared rows]
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
                     const int32_t* grp_off, int T, int k, int E, int n_shared, int d,

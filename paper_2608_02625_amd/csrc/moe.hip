@@ -1,121 +1,260 @@
-// Mixture-of-experts routing for the refiner's FFN: softmax router top-k,
-// dispatch (per-expert row ranges + device tile table for the grouped GEMM)
-// and the weighted combine back into the residual stream.
+// Mixture-of-experts routing for the refiner's FFN: router logits with
+// softmax top-k, dispatch (per-expert row ranges + device tile table for the
+// grouped GEMM) and the weighted combine back into the residual stream.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace {
 
-// One wave per token.  p = softmax(z) over all E experts; the k largest
-// logits are selected (ties -> lower expert id) and their probabilities are
-// renormalised to sum to one.
-__global__ void topk_kernel(const float* __restrict__ logits, int T, int E, int k,
-                            int32_t* __restrict__ ids, float* __restrict__ w) {
-    const int lane = threadIdx.x & 63;
-    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (t >= T) return;
-    const float* z = logits + (int64_t)t * E;
-    float v[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int e = lane + 64 * q;
-        v[q] = (e < E) ? z[e] : -INFINITY;
-    }
-    float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-    m = wave_max(m);
-    float sum = 0.f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) sum += (lane + 64 * q < E) ? __expf(v[q] - m) : 0.f;
-    sum = wave_sum(sum);
+// Router + top-k for 32 tokens per workgroup (16 waves).
+// z^T[e][t] = sum_c Wr[e][c] h[t][c] on v_mfma_f32_32x32x16_bf16 with experts
+// as rows (NB <= 16 blocks of 32) and tokens as columns; the reduction
+// dimension is split over 16 / NB waves per block and the parts are added in a
+// fixed order.  Each wave then selects for 2 tokens; lane r < k
+// records selection r with its rank among this workgroup's selections of the
+// same expert (LDS counter), and the workgroup's per-expert counts go to
+// wg_counts[E][workgroup].  Ranks only order rows inside an expert's group.
+template <int NB>
+__global__ __launch_bounds__(1024) void router_topk_kernel(const bf16_t* __restrict__ h, const bf16_t* __restrict__ Wr,
+                                                          int T, int d, int E, int k, int32_t* __restrict__ ids,
+                                                          float* __restrict__ wts, int32_t* __restrict__ pos,
+                                                          int32_t* __restrict__ wg_counts) {
+    constexpr int NW = 16;                           // waves
+    static_assert(NB >= 1 && NB <= NW, "expert blocks");
+    constexpr int KSPLIT = NW / NB;                  // waves sharing an expert block
+    constexpr int BPW = 1;                           // expert blocks per wave
+    constexpr int EP = NB * 32;                      // padded expert count (LDS row)
+    constexpr int ZROW = EP + 4;                     // row stride: 16-byte aligned, 4 banks of skew
+    __shared__ __attribute__((aligned(16))) float zs[KSPLIT][32][ZROW];
+    __shared__ int lcnt[EP];
 
-    bool sel[4] = {false, false, false, false};
-    int isel[8];
-    float psel[8];
-    float psum = 0.f;
-    for (int r = 0; r < k; ++r) {
-        float bv = -INFINITY;
-        int be = 0x7fffffff;
+    // The wave index is made scalar so that branches on it (the K-batch tail
+    // below) are real branches: an MFMA under an EXEC mask still accumulates.
+    const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
+    const int g = lane >> 5, j = lane & 31;
+    const int t0 = blockIdx.x * 32;
+    const int blk0 = (wave / KSPLIT) * BPW, kc = wave % KSPLIT;
+    // K share of this wave: whole 16-wide steps, the last share may be short or empty.
+    const int kspan = (d / 16 + KSPLIT - 1) / KSPLIT * 16, kbeg = kc * kspan;
+    const int kend = min(kbeg + kspan, d);
+
+    for (int e = threadIdx.x; e < EP; e += NW * 64) lcnt[e] = 0;
+    const bf16_t* hrow = h + (int64_t)min(t0 + j, T - 1) * d + g * 8;
+    const bf16_t* wrow[BPW];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = lane + 64 * q;
-            if (e < E && !sel[q] && (v[q] > bv || be == 0x7fffffff)) {
-                bv = v[q];
-                be = e;
+    for (int b = 0; b < BPW; ++b)                    // rows past E: clamped, their logits unused
+        wrow[b] = Wr + (int64_t)min((blk0 + b) * 32 + j, E - 1) * d + g * 8;
+    f32x16 acc[BPW];
+#pragma unroll
+    for (int b = 0; b < BPW; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
+    // K in batches of U steps; the fragments of batch n+1 are loaded while
+    // the MFMAs of batch n run (steps past the wave's span are clamped loads
+    // whose MFMAs are skipped).
+    constexpr int U = 4;
+    bf16x8 hb[2][U], wa[2][U][BPW];
+    auto load = [&](int buf, int c0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = min(c0 + 16 * u, kend - 16);
+            hb[buf][u] = *reinterpret_cast<const bf16x8*>(hrow + c);
+#pragma unroll
+            for (int b = 0; b < BPW; ++b) wa[buf][u][b] = *reinterpret_cast<const bf16x8*>(wrow[b] + c);
+        }
+    };
+    auto compute = [&](int buf, int c0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c0 + 16 * u < kend) {
+#pragma unroll
+                for (int b = 0; b < BPW; ++b) acc[b] = mfma32x32x16(wa[buf][u][b], hb[buf][u], acc[b]);
+            }
+    };
+    if (kbeg < kend) load(0, kbeg);
+    for (int c0 = kbeg; c0 < kend; c0 += 32 * U) {
+        if (c0 + 16 * U < kend) load(1, c0 + 16 * U);
+        compute(0, c0);
+        if (c0 + 16 * U >= kend) break;
+        if (c0 + 32 * U < kend) load(0, c0 + 32 * U);
+        compute(1, c0 + 16 * U);
+    }
+    // acc[b][e]: expert (blk0+b)*32 + 8*(e/4) + 4*g + e%4, token j
+#pragma unroll
+    for (int b = 0; b < BPW; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zs[kc][j][(blk0 + b) * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = acc[b][e];
+    __syncthreads();
+    // Sum the K parts in a fixed order; logits of experts >= E become -inf.
+    for (int i = threadIdx.x; i < 32 * EP; i += NW * 64) {
+        const int tt = i / EP, e = i - tt * EP;
+        float z = zs[0][tt][e];
+#pragma unroll
+        for (int s = 1; s < KSPLIT; ++s) z += zs[s][tt][e];
+        zs[0][tt][e] = e < E ? z : -INFINITY;
+    }
+    __syncthreads();
+
+    // Top-k per token, one wave per token at a time; lane owns experts
+    // lane + 64q.  p = softmax(z) over the E experts; expert e is selection
+    // r = #{e' : z[e'] > z[e] or (z[e'] == z[e] and e' < e)} if r < k (the k
+    // largest logits, ties -> lower id, in descending order); the selected
+    // probabilities are renormalised to sum to one.
+    constexpr int NQ = (EP + 63) / 64;
+    constexpr int TPW = 32 / NW;                     // tokens per wave
+    for (int i = 0; i < TPW; ++i) {
+        const int tt = wave * TPW + i, t = t0 + tt;
+        const float* z = zs[0][tt];
+        float v[NQ];
+        int rank[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            v[q] = (lane + 64 * q < E) ? z[lane + 64 * q] : -INFINITY;
+            rank[q] = 0;
+        }
+        // z is -inf past E up to a multiple of 4: reads are wave-uniform LDS
+        // broadcasts, four logits at a time.
+        const int E4 = (E + 3) & ~3;
+        float m = -INFINITY;
+#pragma unroll 4
+        for (int e2 = 0; e2 < E4; e2 += 4) {
+            const float4 z4 = *reinterpret_cast<const float4*>(z + e2);
+            const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
+            m = fmaxf(fmaxf(m, fmaxf(zz[0], zz[1])), fmaxf(zz[2], zz[3]));
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    const int e = lane + 64 * q;
+                    rank[q] += (zz[u] > v[q] || (zz[u] == v[q] && e2 + u < e)) ? 1 : 0;
+                }
+        }
+        float p[NQ], own = 0.f;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            p[q] = (lane + 64 * q < E) ? __expf(v[q] - m) : 0.f;
+            own += p[q];
+        }
+        const float sum = wave_sum(own);
+        float psel = 0.f;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            if (rank[q] < k) psel += p[q] / sum;
+        const float psum = wave_sum(psel);
+        if (t < T) {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const int e = lane + 64 * q;
+                if (e < E && rank[q] < k) {
+                    const int64_t o = (int64_t)t * k + rank[q];
+                    ids[o] = e;
+                    wts[o] = p[q] / sum / psum;
+                    pos[o] = atomicAdd(&lcnt[e], 1);
+                }
             }
         }
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            const float ov = __shfl_xor(bv, off, 64);
-            const int oe = __shfl_xor(be, off, 64);
-            if (ov > bv || (ov == bv && oe < be)) {
-                bv = ov;
-                be = oe;
-            }
-        }
-        if (be >= E) be = 0;   // only reachable with non-finite logits; keeps ids in range
-        if ((be & 63) == lane) sel[be >> 6] = true;
-        isel[r] = be;
-        psel[r] = __expf(bv - m) / sum;
-        psum += psel[r];
     }
-    if (lane == 0) {
-        for (int r = 0; r < k; ++r) {
-            ids[(int64_t)t * k + r] = isel[r];
-            w[(int64_t)t * k + r] = psel[r] / psum;
-        }
-    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += NW * 64) wg_counts[(int64_t)e * gridDim.x + blockIdx.x] = lcnt[e];
 }
 
-// One workgroup (1024 threads) builds the whole dispatch from the top-k ids:
-// groups are the E routed experts (rows = tokens routed there) followed by
-// n_shared shared experts (T rows each).  Writes grp_off[0..G], the tile table
-// (group, m0) of the grouped GEMM and its length, slot[t][j] (the row of
-// token t's j-th expert) and a_rows[row] = token.  Histogram and cursors live
-// in LDS; the row order inside a group depends on atomic order but no result
-// does (rows are computed independently and combined by slot).
-__global__ __launch_bounds__(1024) void dispatch_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
-                                                        int n_shared, int bm, int32_t* __restrict__ grp_off,
-                                                        int2* __restrict__ tile_tab, int32_t* __restrict__ n_tiles,
-                                                        int32_t* __restrict__ slot, int32_t* __restrict__ a_rows) {
-    __shared__ int cnt[512];
-    __shared__ int off[513];
-    __shared__ int toff[513];
+// Exclusive scan of n <= 512 non-negative ints held in LDS, by one wave;
+// out[n] receives the total.
+__device__ void wave_scan512(const int* in, int* out, int n) {
+    const int lane = threadIdx.x & 63;
+    int v[8], run = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int idx = lane * 8 + i;
+        v[i] = idx < n ? in[idx] : 0;
+        run += v[i];
+    }
+    int incl = run;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int o = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += o;
+    }
+    int excl = incl - run;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int idx = lane * 8 + i;
+        if (idx < n) out[idx] = excl;
+        excl += v[i];
+    }
+    if (lane == 63) out[n] = incl;
+}
+
+// Dispatch plan (one workgroup of 16 waves).  For every expert e, wave e % 16
+// turns the row wg_counts[e][.] into exclusive offsets over the router
+// workgroups (in place) and keeps the row total.  Groups are the E routed
+// experts followed by n_shared shared experts of T rows each; their sizes are
+// scanned into grp_off[0..G], and the tile table (group, m0) of the grouped
+// GEMM and its length are written.
+__global__ __launch_bounds__(1024) void dispatch_plan_kernel(int T, int E, int n_shared, int nwg, int bm,
+                                                             int32_t* __restrict__ wg_counts,
+                                                             int32_t* __restrict__ grp_off, int2* __restrict__ tile_tab,
+                                                             int32_t* __restrict__ n_tiles) {
+    __shared__ int cnt[512], off[513], ntl[512], toff[513];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int G = E + n_shared;
-    const int nr = T * k;
-    for (int g = threadIdx.x; g < G; g += blockDim.x) cnt[g] = (g < E) ? 0 : T;
-    __syncthreads();
-    for (int i = threadIdx.x; i < nr; i += blockDim.x) atomicAdd(&cnt[ids[i]], 1);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int o = 0, to = 0;
-        for (int g = 0; g < G; ++g) {
-            off[g] = o;
-            toff[g] = to;
-            o += cnt[g];
-            to += (cnt[g] + bm - 1) / bm;
+    for (int e = wave; e < E; e += 16) {
+        int32_t* col = wg_counts + (int64_t)e * nwg;
+        int carry = 0;
+        for (int w0 = 0; w0 < nwg; w0 += 256) {
+            int v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int wi = w0 + 64 * q + lane;
+                v[q] = wi < nwg ? col[wi] : 0;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int wi = w0 + 64 * q + lane;
+                int incl = v[q];
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int u = __shfl_up(incl, o, 64);
+                    if (lane >= o) incl += u;
+                }
+                if (wi < nwg) col[wi] = carry + incl - v[q];
+                carry += __shfl(incl, 63, 64);
+            }
         }
-        off[G] = o;
-        toff[G] = to;
-        *n_tiles = to;
-        grp_off[G] = o;
+        if (lane == 0) cnt[e] = carry;
     }
+    for (int gi = E + threadIdx.x; gi < G; gi += blockDim.x) cnt[gi] = T;
     __syncthreads();
-    for (int g = threadIdx.x; g < G; g += blockDim.x) {
-        grp_off[g] = off[g];
-        const int nt = toff[g + 1] - toff[g];
-        for (int t = 0; t < nt; ++t) tile_tab[toff[g] + t] = make_int2(g, t * bm);
-        cnt[g] = 0;                                   // reused as the per-group cursor
-    }
+    for (int gi = threadIdx.x; gi < G; gi += blockDim.x) ntl[gi] = (cnt[gi] + bm - 1) / bm;
     __syncthreads();
-    for (int i = threadIdx.x; i < nr; i += blockDim.x) {
-        const int e = ids[i];
-        const int s = off[e] + atomicAdd(&cnt[e], 1);
+    if (wave == 0) wave_scan512(cnt, off, G);
+    else if (wave == 1) wave_scan512(ntl, toff, G);
+    __syncthreads();
+    for (int gi = threadIdx.x; gi <= G; gi += blockDim.x) grp_off[gi] = off[gi];
+    if (threadIdx.x == 0) *n_tiles = toff[G];
+    for (int gi = threadIdx.x; gi < G; gi += blockDim.x)
+        for (int t = 0; t < ntl[gi]; ++t) tile_tab[toff[gi] + t] = make_int2(gi, t * bm);
+}
+
+// Thread i < T*k turns the rank pos[i] of selection i into its row
+// slot[i] = grp_off[e] + (offset of its router workgroup at e) + pos[i]
+// (in place) and sets a_rows[slot] = token; the rest fill the shared groups.
+__global__ __launch_bounds__(256) void dispatch_scatter_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                               int n_shared, int nwg, const int32_t* __restrict__ wg_off,
+                                                               const int32_t* __restrict__ grp_off,
+                                                               int32_t* __restrict__ slot, int32_t* __restrict__ a_rows) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    const int nr = T * k;
+    if (i < nr) {
+        const int t = i / k, e = ids[i];
+        const int s = grp_off[e] + wg_off[(int64_t)e * nwg + (t >> 5)] + slot[i];
         slot[i] = s;
-        a_rows[s] = i / k;
-    }
-    for (int i = threadIdx.x; i < n_shared * T; i += blockDim.x) {
-        const int sh = i / T, t = i - sh * T;
-        a_rows[off[E + sh] + t] = t;
+        a_rows[s] = t;
+    } else if (i < nr + n_shared * T) {
+        const int r = i - nr, sh = r / T, t = r - sh * T;
+        a_rows[grp_off[E + sh] + t] = t;
     }
 }
 
@@ -162,14 +301,32 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
 
 }  // namespace
 
-void launch_topk(const float* logits, int T, int E, int k, int32_t* ids, float* w, hipStream_t st) {
-    hipLaunchKernelGGL(topk_kernel, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, k, ids, w);
+hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, int E, int k, int32_t* ids,
+                              float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st) {
+    if (E < 1 || E > 256 || k < 1 || k > 8 || k > E || d % 64 != 0 || T < 1) return hipErrorInvalidValue;
+    const dim3 grid((T + 31) / 32), block(1024);
+    if (E <= 32)
+        hipLaunchKernelGGL(router_topk_kernel<1>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+    else if (E <= 64)
+        hipLaunchKernelGGL(router_topk_kernel<2>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+    else if (E <= 128)
+        hipLaunchKernelGGL(router_topk_kernel<4>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+    else
+        hipLaunchKernelGGL(router_topk_kernel<8>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+    return hipGetLastError();
 }
 
-void launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared, int bm, int32_t* grp_off,
-                     int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows, hipStream_t st) {
-    hipLaunchKernelGGL(dispatch_kernel, dim3(1), dim3(1024), 0, st, ids, T, k, E, n_shared, bm, grp_off,
-                       tile_tab, n_tiles, slot, a_rows);
+hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared, int bm, int32_t* wg_counts,
+                           int32_t* grp_off, int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows,
+                           hipStream_t st) {
+    if (E + n_shared > 512) return hipErrorInvalidValue;
+    const int nwg = (T + 31) / 32;
+    hipLaunchKernelGGL(dispatch_plan_kernel, dim3(1), dim3(1024), 0, st, T, E, n_shared, nwg, bm, wg_counts,
+                       grp_off, tile_tab, n_tiles);
+    const int64_t n = (int64_t)T * k + (int64_t)n_shared * T;
+    hipLaunchKernelGGL(dispatch_scatter_kernel, dim3((unsigned)std::max<int64_t>(1, (n + 255) / 256)), dim3(256), 0,
+                       st, ids, T, k, E, n_shared, nwg, wg_counts, grp_off, slot, a_rows);
+    return hipGetLastError();
 }
 
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
