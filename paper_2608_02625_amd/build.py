@@ -38,11 +38,25 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _device_asm(src: str) -> str:
+    """gfx950 assembly of one source (kept for the static checks in tests/)."""
+    asm = os.path.join(BUILD, src.replace(".hip", ".s"))
+    cmd = [_hipcc(), *CFLAGS, "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", asm]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stderr}")
+    return asm
+
+
 def build(jobs: int | None = None) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    jobs = jobs or min(len(SOURCES), os.cpu_count() or 4)
+    jobs = jobs or min(2 * len(SOURCES), os.cpu_count() or 4)
     with ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        obj_f = [ex.submit(_compile, s) for s in SOURCES]
+        asm_f = [ex.submit(_device_asm, s) for s in SOURCES]
+        objs = [f.result() for f in obj_f]
+        for f in asm_f:
+            f.result()
     tmp = OUT + f".tmp{os.getpid()}"
     cmd = [_hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
