@@ -202,7 +202,7 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
         w.hexp = add((int64_t)w.rows_total * c.expert_ffn_dim * 2);
         w.y = add((int64_t)w.rows_total * d * 2);
     }
-    w.n_vtiles = (c.vocab + kHeadBM - 1) / kHeadBM;
+    w.n_vtiles = 2 * ((c.vocab + kHeadBM - 1) / kHeadBM);   // LM-head partials per half tile
     w.hfin = add(R * d * 2);
     w.partials = add((int64_t)w.n_vtiles * R * 16);
     w.top1 = add(R * 4);
@@ -405,7 +405,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = a_rows;
         a.out = hexp;
         a.ldo = F;
-        a.variant = 2;
+        a.variant = 5;                                  // third stage for the streamed expert weights (B)
         TRY(gemm(x, "gemm_expert_gate_up", a, EPI_SWIGLU, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     {
@@ -441,7 +441,7 @@ dlm_status run_head(Ctx& x, int32_t* top1, float* conf, float* maxlogit, float* 
     GemmArgs a = gemm_args(x.wt(x.m->plan.lm), c.d_model, hfin, c.d_model, c.vocab, x.R, c.d_model);
     a.partials = x.at<float4>(x.w.partials);
     a.group_m = 4;
-    a.variant = 2;
+    a.variant = 6;                                      // third stage for the streamed vocabulary rows (A)
     TRY(gemm(x, "gemm_lm_head", a, EPI_LMHEAD, false, kHeadBM, kHeadBN, 0));
     LAUNCH(x, "lmhead_merge", launch_lmhead_merge(a.partials, x.w.n_vtiles, x.R, top1, conf, maxlogit, x.st));
     if (logits_out) {

@@ -26,7 +26,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int BM, int BN, int BK, int STAGES, int NW>
+template <int BM, int BN, int BK, int SA, int SB, int NW>
 struct TileCfg {
     static constexpr int NT = NW * 64;                   // threads
     static constexpr int WM = BM / 2, WN = BN / (NW / 2);
@@ -35,11 +35,20 @@ struct TileCfg {
     static constexpr int CPR = BK / 8;                   // 16-byte chunks per row
     static constexpr int KS = BK / 16;                   // MFMA K steps per tile
     static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
-    static constexpr int STAGE = A_BYTES + B_BYTES;
-    static constexpr int LDS = STAGES * STAGE;
+    static constexpr int LDS = SA * A_BYTES + SB * B_BYTES;
     static constexpr int A_INSTR = A_BYTES / 1024 / NW;  // 1 KB DMA blocks per wave
     static constexpr int B_INSTR = B_BYTES / 1024 / NW;
-    static constexpr int NI = A_INSTR + B_INSTR;         // DMA instructions per wave per tile
+    // The operand with fewer stages is copied first in every round of copies
+    // (S = shallow, D = deep).  Waiting until at most N copies are pending
+    // (copies complete in order) then guarantees:
+    //   N_TOP:  K tile 0 of both operands landed (after the first round);
+    //   N_LOOP: K tile kt+1 of both landed, at the barrier of tile kt.
+    static constexpr int SS = SA < SB ? SA : SB, SD = SA < SB ? SB : SA;
+    static constexpr int NI_S = SA <= SB ? A_INSTR : B_INSTR, NI_D = SA <= SB ? B_INSTR : A_INSTR;
+    static constexpr int N_TOP = (SS - 1) * NI_S + (SD - 1) * NI_D;
+    static constexpr int CNT_S = NI_D + (SS - 2) * (NI_S + NI_D), CNT_D = (SD - 2) * (NI_S + NI_D);
+    static constexpr int N_LOOP = CNT_S < CNT_D ? CNT_S : CNT_D;
+    static_assert(SS >= 2, "at least two stages per operand");
 };
 
 // XOR key of the 16-byte chunks of a tile row: consecutive rows read by one
@@ -132,13 +141,10 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
     }
 }
 
-template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
+template <int BM, int BN, int BK, int SA, int SB, int NW, int EPI, bool GROUPED>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void gemm_kernel(GemmArgs a) {
-    using T = TileCfg<BM, BN, BK, STAGES, NW>;
-    // LM-head partial merge buffer, past the K stages (which may already hold
-    // the next tile's copies while this tile's epilogue runs).
-    constexpr int XBUF = EPI == EPI_LMHEAD ? (NW / 2) * T::TN * 32 * 16 : 0;
-    __shared__ __attribute__((aligned(16))) char smem[T::LDS + XBUF];
+    using T = TileCfg<BM, BN, BK, SA, SB, NW>;
+    __shared__ __attribute__((aligned(16))) char smem[T::LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);   // scalar: wave-level branches stay branches
     const int wm = wave / (NW / 2), wn = wave % (NW / 2);
@@ -199,11 +205,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     // offset, so the copies cost no vector ALU work.  The XOR swizzle of the
     // 16-byte chunks is applied on the global side: the lane that fills
     // physical chunk pc of row r fetches logical chunk pc ^ key(r).
-    // LDS = [A stage 0 .. A stage S-1 | B stage 0 .. B stage S-1]; fragment
-    // reads are a per-lane base plus a compile-time offset.
+    // LDS = [A stage 0 .. SA-1 | B stage 0 .. SB-1]; fragment reads are a
+    // per-lane base plus a compile-time offset.
     constexpr int CPR = T::CPR;
     constexpr int RPB = 64 / CPR;                               // tile rows per 1 KB block
-    constexpr int B_BASE = STAGES * T::A_BYTES;
+    constexpr int B_BASE = SA * T::A_BYTES;
     const int wv = wave;
     const int rin = lane / CPR, pc = lane % CPR;
     const bool gather = GROUPED && a.a_rows != nullptr;
@@ -231,14 +237,37 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     typedef __attribute__((address_space(3))) char lds_char;
     typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
     auto lds_at = [&](int off) { return (lds_ptr_t)((lds_char*)lds + off); };
-    auto issue = [&](int kt, int stage) {                        // tile kt -> LDS stage
-        const int soff = kt * (BK * 2);
-        const int a_dst = stage * T::A_BYTES + wv * T::A_INSTR * 1024;
-        const int b_dst = B_BASE + stage * T::B_BYTES + wv * T::B_INSTR * 1024;
+    auto issue_a = [&](int kt, int stage) {                      // A of K tile kt -> A stage
+        const int dst = stage * T::A_BYTES + wv * T::A_INSTR * 1024;
 #pragma unroll
-        for (int p = 0; p < T::A_INSTR; ++p) lds_dma16_buf(a_rsrc, a_off[p], soff, lds_at(a_dst + p * 1024));
+        for (int p = 0; p < T::A_INSTR; ++p) lds_dma16_buf(a_rsrc, a_off[p], kt * (BK * 2), lds_at(dst + p * 1024));
+    };
+    auto issue_b = [&](int kt, int stage) {
+        const int dst = B_BASE + stage * T::B_BYTES + wv * T::B_INSTR * 1024;
 #pragma unroll
-        for (int p = 0; p < T::B_INSTR; ++p) lds_dma16_buf(b_rsrc, b_off[p], soff, lds_at(b_dst + p * 1024));
+        for (int p = 0; p < T::B_INSTR; ++p) lds_dma16_buf(b_rsrc, b_off[p], kt * (BK * 2), lds_at(dst + p * 1024));
+    };
+    // One round of copies: the shallow operand first (see TileCfg).
+    auto issue = [&](int kt_a, int st_a, int kt_b, int st_b) {
+        if constexpr (SA <= SB) {
+            issue_a(kt_a, st_a);
+            issue_b(kt_b, st_b);
+        } else {
+            issue_b(kt_b, st_b);
+            issue_a(kt_a, st_a);
+        }
+    };
+    auto prologue = [&](int nk) {                                // first K tiles of a tile
+#pragma unroll
+        for (int t = 0; t < T::SD; ++t) {
+            if constexpr (SA <= SB) {
+                if (t < SA) issue_a(min(t, nk - 1), t);
+                issue_b(min(t, nk - 1), t);
+            } else {
+                if (t < SB) issue_b(min(t, nk - 1), t);
+                issue_a(min(t, nk - 1), t);
+            }
+        }
     };
 
     f32x16 acc[T::TM][T::TN];
@@ -251,12 +280,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const int fa0 = swz<CPR>(wm * T::WM + (lane & 31), lane >> 5);
     const int fb0 = swz<CPR>(wn * T::WN + (lane & 31), lane >> 5);
     bf16x8 ra[T::KS][T::TM], rb[T::KS][T::TN];
-    // Per-lane bases of the stage being read: fa_s = fa0 + stage * A_BYTES
+    // Per-lane bases of the stages being read: fa_s = fa0 + stage * A_BYTES
     // (the stage term sits above bit 14, so the slot XOR below commutes with it).
     int fa_s = fa0, fb_s = B_BASE + fb0;
-    auto set_stage = [&](int stage) {
-        fa_s = fa0 + stage * T::A_BYTES;
-        fb_s = B_BASE + fb0 + stage * T::B_BYTES;
+    auto set_stage = [&](int st_a, int st_b) {
+        fa_s = fa0 + st_a * T::A_BYTES;
+        fb_s = B_BASE + fb0 + st_b * T::B_BYTES;
     };
     auto read_slot = [&](int ks) {                               // fragments of step ks
         const int fa = fa_s ^ (ks * 32), fb = fb_s ^ (ks * 32);
@@ -267,23 +296,32 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         for (int j = 0; j < T::TN; ++j)
             rb[ks][j] = *(lds_frag*)((lds_char*)lds + fb + j * 32 * T::ROW);
     };
+    // The SwiGLU epilogue takes the accumulators transposed (operands
+    // swapped): a lane then holds 4 consecutive output features of one row,
+    // stored as one 8-byte write.  The other epilogues keep rows in the
+    // accumulator's 4-element groups (consecutive lanes = consecutive columns:
+    // fully coalesced 2-row stores).
+    constexpr bool TACC = EPI == EPI_SWIGLU;
     auto mfmas = [&](int ks) {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-            for (int j = 0; j < T::TN; ++j) acc[i][j] = mfma32x32x16(ra[ks][i], rb[ks][j], acc[i][j]);
+            for (int j = 0; j < T::TN; ++j)
+                acc[i][j] = TACC ? mfma32x32x16(rb[ks][j], ra[ks][i], acc[i][j])
+                                 : mfma32x32x16(ra[ks][i], rb[ks][j], acc[i][j]);
     };
     constexpr int NR = T::TM + T::TN, NM = T::TM * T::TN;
     constexpr int PRE = T::KS / 2;          // fragment steps of a tile run before its barrier
 
-    // Software pipeline over K tiles (tile kt lives in LDS stage kt % STAGES;
+    // Software pipeline over K tiles (A of tile kt lives in A stage kt % SA,
+    // B in B stage kt % SB;
     // registers hold every fragment of the tile being multiplied).  Per tile,
     // in phases the compiler may not reorder across:
     //   [steps 0 .. PRE-1 of tile kt ran at the end of the previous tile]
     //   wait until this wave's copy of tile kt+1 landed (its reads of tile kt
     //   finished long ago); barrier: tile kt+1 is complete in LDS and the
     //   stage of tile kt is free;
-    //   step PRE      | copy of tile kt+STAGES into the freed stage
+    //   step PRE      | copies of A tile kt+SA and B tile kt+SB into the freed stages
     //                 | reads of tile kt+1 slots 0 .. PRE-1 (their steps are done)
     //   step s > PRE  | reads of slot s-1
     //   step 0 of kt+1 | reads of slot KS-1
@@ -295,8 +333,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const int nk = a.K / BK;
     TileIdx cur = decode(L);
     setup_copies(cur);
-#pragma unroll
-    for (int t = 0; t < STAGES; ++t) issue(min(t, nk - 1), t);
+    prologue(nk);
 
     // ---------------------------------------------------------------- per tile
     while (true) {
@@ -307,14 +344,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         for (int j = 0; j < T::TN; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-    wait_vmcnt<(STAGES - 1) * T::NI>();     // K tile 0 landed, later ones may fly
+    wait_vmcnt<T::N_TOP>();                 // K tile 0 landed, later ones may fly
     __syncthreads();
     // In grouped mode the last row tile of a group is often partly empty; a
     // wave whose rows all lie past the group's end skips its MFMAs (and
     // fragment reads) but still copies and meets every barrier.
     auto run = [&](auto active) {
         constexpr bool ACTIVE = decltype(active)::value;
-        set_stage(0);
+        set_stage(0, 0);
         if constexpr (ACTIVE) {
 #pragma unroll
             for (int ks = 0; ks < T::KS; ++ks) read_slot(ks);
@@ -323,18 +360,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         }
         sched_fence();
 
-        int st = 0;                             // stage of tile kt
+        int sa = 0, sb = 0;                     // stages of tile kt
         for (int kt = 0; kt < nk - 1; ++kt) {
-            const int sn = st + 1 == STAGES ? 0 : st + 1;
-            wait_vmcnt<(STAGES - 2) * T::NI>();                     // own copy of tile kt+1 landed
+            const int na = sa + 1 == SA ? 0 : sa + 1, nb = sb + 1 == SB ? 0 : sb + 1;
+            wait_vmcnt<T::N_LOOP>();                                // own copies of tile kt+1 landed
             __syncthreads();
-            set_stage(sn);
+            set_stage(na, nb);
             sched_fence();
-            // step PRE | copy of tile kt+STAGES | reads of slots 0 .. PRE-1 of tile kt+1
+            // step PRE | copies of tiles kt+SA / kt+SB | reads of slots 0 .. PRE-1 of tile kt+1
             if constexpr (ACTIVE) mfmas(PRE);
-            issue(min(kt + STAGES, nk - 1), st);
+            issue(min(kt + SA, nk - 1), sa, min(kt + SB, nk - 1), sb);
             if constexpr (!ACTIVE) {
-                st = sn;
+                sa = na;
+                sb = nb;
                 continue;
             }
 #pragma unroll
@@ -344,7 +382,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             for (int r = 0; r < NM; ++r) {
                 sched_group<0x008, 1>();
 #pragma unroll
-                for (int c = r * T::NI / NM; c < (r + 1) * T::NI / NM; ++c) sched_group<0x020, 1>();
+                for (int c = r * (T::A_INSTR + T::B_INSTR) / NM; c < (r + 1) * (T::A_INSTR + T::B_INSTR) / NM; ++c)
+                    sched_group<0x020, 1>();
 #pragma unroll
                 for (int c = r * NRD / NM; c < (r + 1) * NRD / NM; ++c) sched_group<0x100, 1>();
             }
@@ -373,7 +412,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
 #pragma unroll
             for (int ks = 1; ks < PRE; ++ks) mfmas(ks);
             sched_fence();
-            st = sn;
+            sa = na;
+            sb = nb;
         }
         if constexpr (ACTIVE) {
 #pragma unroll
@@ -391,17 +431,23 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     if (more) {
         cur = decode(L_next);
         setup_copies(cur);
-#pragma unroll
-        for (int t = 0; t < STAGES; ++t) issue(min(t, nk - 1), t);
+        prologue(nk);
     }
 
     // ---------------------------------------------------------------- epilogues
-    // acc[i][j][e] holds C[row][col] with
+    // TACC: acc[i][j][4q + r] holds C[row][col] with
+    //   row = wm*WM + i*32 + lane%32,  col = wn*WN + j*32 + 8q + 4*(lane/32) + r.
+    // otherwise acc[i][j][e] holds C[row][col] with
     //   row = wm*WM + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = wn*WN + j*32 + lane%32.
     const int lrow0 = wm * T::WM + 4 * (lane >> 5);
     const int lcol0 = wn * T::WN + (lane & 31);
-
+    const int trow = m0 + wm * T::WM + (lane & 31);              // TACC row of block i = 0
+    const int tcol = n0 + wn * T::WN + 4 * (lane >> 5);          // TACC column of j = 0, q = 0
+    // 4-column groups are stored whole when they lie inside N and rows are
+    // 16-byte (f32) / 8-byte (bf16) aligned.
+    const bool vec = (a.ldo & 3) == 0;
     const bool full_tile = m0 + BM <= rows && n0 + BN <= a.N;
+
     if constexpr (EPI == EPI_RESID) {
         // out[row][col] += acc: per 32-row block all 16 x TN loads are issued
         // before the adds and stores.
@@ -461,25 +507,36 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                 }
             }
     } else if constexpr (EPI == EPI_SWIGLU) {
-        // Physical columns alternate 32 gate / 32 up; the pair (j, j+1) shares f.
+        // Physical columns alternate 32 gate / 32 up: blocks (j, j+1) hold the
+        // gate and up values of the same 32 features; 4 consecutive features
+        // per lane leave as one 8-byte store.
 #pragma unroll
-        for (int i = 0; i < T::TM; ++i)
+        for (int i = 0; i < T::TM; ++i) {
+            const int r = trow + i * 32;
+            if (r >= rows) continue;
+            bf16_t* orow = reinterpret_cast<bf16_t*>(a.out) + (GROUPED ? (int64_t)row_base + r : r) * a.ldo;
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int rl = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-                if (rl >= rows) continue;
-                const int64_t orow = GROUPED ? (int64_t)row_base + rl : rl;
+            for (int j = 0; j < T::TN; j += 2) {
+                const int c0 = n0 + wn * T::WN + j * 32;                // first gate column of the pair
+                if (c0 >= a.N) continue;
 #pragma unroll
-                for (int j = 0; j < T::TN; j += 2) {
-                    const int c0 = n0 + wn * T::WN + j * 32;
-                    if (c0 >= a.N) continue;
-                    const int f = (c0 >> 1) + (lane & 31);
-                    const float gt = acc[i][j][e];
-                    const float up = acc[i][j + 1][e];
-                    const float h = gt / (1.f + __expf(-gt)) * up;
-                    reinterpret_cast<bf16_t*>(a.out)[orow * a.ldo + f] = f32_to_bf16(h);
+                for (int q = 0; q < 4; ++q) {
+                    float hv[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const float gt = acc[i][j][4 * q + t], up = acc[i][j + 1][4 * q + t];
+                        hv[t] = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
+                    }
+                    const int f = (c0 >> 1) + 8 * q + 4 * (lane >> 5);
+                    if (vec)
+                        *reinterpret_cast<u32x2*>(orow + f) = u32x2{pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
+                    else {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) orow[f + t] = f32_to_bf16(hv[t]);
+                    }
                 }
             }
+        }
     } else if constexpr (EPI == EPI_QKV) {
         static_assert(T::WM % 128 == 0, "a wave's rows must cover whole heads");
         if (a.head_dim == 128)
@@ -488,7 +545,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             qkv_epilogue<T::TM, T::TN, 64>(a, acc, m0, n0, lrow0, lcol0);
     } else if constexpr (EPI == EPI_LMHEAD) {
         // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
-        // sum exp(z - max)) over this tile's BM vocabulary rows.
+        // sum exp(z - max)) over each half tile's BM/2 vocabulary rows.
         SoftmaxPartial part[T::TN];
 #pragma unroll
         for (int j = 0; j < T::TN; ++j) {
@@ -523,25 +580,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             q.s = __shfl_xor(p.s, 32, 64);
             part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
         }
-        // Merge the two waves that share these token columns (wm = 0, 1).
-        float4* xbuf = reinterpret_cast<float4*>(smem + T::LDS);
-        if (wm == 1 && lane < 32) {
-#pragma unroll
-            for (int j = 0; j < T::TN; ++j)
-                xbuf[(wn * T::TN + j) * 32 + lane] =
-                    make_float4(part[j].m, __int_as_float(part[j].idx), part[j].s, 0.f);
-        }
-        __syncthreads();
-        if (wm == 0 && lane < 32) {
-            const int tile_m = m0 / BM;
+        // One partial per (BM/2-row half tile, token): the two wave rows
+        // (wm = 0, 1) write separately and the merge kernel combines them.
+        if (lane < 32) {
+            const int half = (m0 / BM) * 2 + wm;
 #pragma unroll
             for (int j = 0; j < T::TN; ++j) {
                 const int c = n0 + lcol0 + j * 32;
-                if (c >= a.N) continue;
-                const float4 o = xbuf[(wn * T::TN + j) * 32 + lane];
-                SoftmaxPartial other{o.x, __float_as_int(o.y), o.z};
-                SoftmaxPartial r = sp_merge(part[j], other);
-                a.partials[(int64_t)tile_m * a.N + c] = make_float4(r.m, __int_as_float(r.idx), r.s, 0.f);
+                if (c < a.N)
+                    a.partials[(int64_t)half * a.N + c] =
+                        make_float4(part[j].m, __int_as_float(part[j].idx), part[j].s, 0.f);
             }
         }
     }
@@ -550,12 +598,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     }
 }
 
-template <int BM, int BN, int BK, int STAGES, int NW, int EPI, bool GROUPED>
+template <int BM, int BN, int BK, int SA, int SB, int NW, int EPI, bool GROUPED>
 hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     if constexpr (EPI == EPI_QKV && (BM / 2) % 128 != 0) {
         return hipErrorInvalidValue;                       // RoPE pairs must stay inside one wave
     } else {
-    auto kernel = gemm_kernel<BM, BN, BK, STAGES, NW, EPI, GROUPED>;
+    auto kernel = gemm_kernel<BM, BN, BK, SA, SB, NW, EPI, GROUPED>;
     // Workgroups that fit on the device at once (a multiple of 8, one share
     // per XCD); a persistent grid of at most that many walks all tiles.
     static int resident = 0;
@@ -578,25 +626,31 @@ hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     }
 }
 
-// Tile configurations: BM x BN x BK with STAGES LDS stages (1 workgroup/CU
-// for the 256-row tiles; 128x128 and 128x64 leave room for two).
+// Tile configurations: BM x BN x BK, SA / SB LDS stages for A / B, NW waves.
+// variant 0: 4 waves; 1: alternative stage/BK choices; 2: 8 waves, 2+2
+// stages; 5: 8 waves with a third B stage (B streamed from far memory, e.g.
+// expert weights); 6: 8 waves with a third A stage (A streamed, e.g. the LM
+// head's vocabulary rows).  The 256x256 8-wave tiles with a third stage use
+// all 160 KB of LDS.
 template <int EPI, bool GROUPED>
 hipError_t launch_tiles(const GemmArgs& a, int bm, int bn, int max_tiles, hipStream_t st) {
     if (a.variant == 1) {
-        if (bm == 256 && bn == 256) return launch_t<256, 256, 32, 4, 4, EPI, GROUPED>(a, max_tiles, st);
-        if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 3, 4, EPI, GROUPED>(a, max_tiles, st);
-        if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+        if (bm == 256 && bn == 256) return launch_t<256, 256, 32, 4, 4, 4, EPI, GROUPED>(a, max_tiles, st);
+        if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 3, 3, 4, EPI, GROUPED>(a, max_tiles, st);
+        if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
         return hipErrorInvalidValue;
     }
-    if (a.variant == 2) {
-        if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 8, EPI, GROUPED>(a, max_tiles, st);
-        return hipErrorInvalidValue;
+    if (bm == 256 && bn == 256) {
+        if (a.variant == 2) return launch_t<256, 256, 64, 2, 2, 8, EPI, GROUPED>(a, max_tiles, st);
+        if (a.variant == 5) return launch_t<256, 256, 64, 2, 3, 8, EPI, GROUPED>(a, max_tiles, st);
+        if (a.variant == 6) return launch_t<256, 256, 64, 3, 2, 8, EPI, GROUPED>(a, max_tiles, st);
     }
-    if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 3, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 256) return launch_t<128, 256, 64, 3, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 64) return launch_t<128, 64, 64, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (a.variant != 0) return hipErrorInvalidValue;
+    if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 3, 3, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 256) return launch_t<128, 256, 64, 3, 3, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 128 && bn == 64) return launch_t<128, 64, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
     return hipErrorInvalidValue;
 }
 

@@ -55,7 +55,7 @@ struct GemmArgs {
     bf16_t* v;
     const float2* rope;       // [S][hd/2] (cos, sin)
     int seq, n_heads, n_kv, head_dim;
-    // EPI_LMHEAD: partials [M/BM tiles][N] (m, idx, s) stored as float4
+    // EPI_LMHEAD: partials [2 * ceil(M/BM) half tiles][N] (m, idx, s) stored as float4
     float4* partials;
 };
 

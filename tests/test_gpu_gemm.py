@@ -18,6 +18,11 @@ pytestmark = pytest.mark.gpu
     (513, 129, 256, (128, 128)),
     (130, 70, 64, (128, 64)),
     (1, 1, 64, (128, 64)),
+    # 8-wave 256x256 tiles: 2+2 stages, a third B stage, a third A stage
+    (600, 520, 640, ((2 << 16) | 256, 256)),
+    (600, 520, 640, ((5 << 16) | 256, 256)),
+    (777, 300, 1088, ((6 << 16) | 256, 256)),
+    (256, 256, 64, ((5 << 16) | 256, 256)),
 ])
 def test_gemm_matches_fp32_reference(m, n, k, tile):
     need_gpu()
