@@ -141,10 +141,11 @@ def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = True):
     T = h.shape[0]
     ids, w, gap = route(h, L["w_router"], k, decide_bf16)
     out = np.zeros_like(h)
-    for e, (wg, wu, wd) in enumerate(L["experts"]):
+    for e in range(len(L["experts"])):
         rows, slot = np.nonzero(ids == e)
         if rows.size == 0:
-            continue
+            continue                      # an expert's weights are only read if a token uses it
+        wg, wu, wd = L["experts"][e]
         y = swiglu(h[rows], wg, wu, wd)
         out[rows] += w[rows, slot][:, None] * y
     for (wg, wu, wd) in L["shared"]:
@@ -179,6 +180,33 @@ def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True):
         info["route_gap"] = gap.reshape(B, S)
         info["route_ids"] = ids.reshape(B, S, -1)
     x += ffn.reshape(B, S, d)
+    return x, info
+
+
+def layer_forward_rows(shape, L: dict, x_seq: np.ndarray, rows: np.ndarray, decide_bf16: bool = True):
+    """The block of layer_forward for one sequence x_seq [S, d], evaluated only
+    at the positions `rows`: keys and values come from all S positions, the
+    queries and everything after attention (which is per position) from the
+    selected ones.  Returns (x [len(rows), d], info for those rows)."""
+    S, d = x_seq.shape
+    H, KV, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
+    rows = np.asarray(rows)
+    x_seq = x_seq.astype(F64)
+    h = rms_norm(x_seq, L["g1"], shape.norm_eps)
+    q = (h[rows] @ L["wq"].astype(F64).T).reshape(len(rows), H, hd)
+    kk = (h @ L["wk"].astype(F64).T).reshape(S, KV, hd)
+    v = (h @ L["wv"].astype(F64).T).reshape(S, KV, hd)
+    q = rope(q, rows, shape.rope_theta)
+    kk = rope(kk, np.arange(S), shape.rope_theta)
+    x = x_seq[rows] + attention(q, kk, v).reshape(len(rows), H * hd) @ L["wo"].astype(F64).T
+    h2 = rms_norm(x, L["g2"], shape.norm_eps)
+    info = {"route_gap": None, "route_ids": None}
+    if shape.n_experts == 0:
+        x = x + swiglu(h2, L["w_gate"], L["w_up"], L["w_down"])
+    else:
+        ffn, ids, gap = moe_ffn(h2, L, shape.top_k, decide_bf16)
+        x = x + ffn
+        info["route_gap"], info["route_ids"] = gap, ids
     return x, info
 
 

@@ -113,6 +113,27 @@ def weight_values_at(seed: int, tid: int, idx: np.ndarray, init_std: float, scal
     return to_weight_values(irwin_hall_at(seed, tid, idx), scale_constant(init_std, scale))
 
 
+class _Experts:
+    """Expert (gate, up, down) weight triples generated when indexed (the
+    flash-scale slice has 256 experts of 19M weights each per layer)."""
+
+    def __init__(self, make, n: int, cache: bool):
+        self._make, self._n = make, n
+        self._cache = {} if cache else None
+
+    def __len__(self):
+        return self._n
+
+    def __getitem__(self, e: int):
+        if not 0 <= e < self._n:
+            raise IndexError(e)
+        if self._cache is None:
+            return self._make(e)
+        if e not in self._cache:
+            self._cache[e] = self._make(e)
+        return self._cache[e]
+
+
 class OracleWeights:
     """Lazily regenerated refiner weights for one (shape, seed)."""
 
@@ -176,10 +197,9 @@ class OracleWeights:
         else:
             F = s.expert_ffn_dim
             L["w_router"] = m(K_ROUTER, s.n_experts, d)
-            L["experts"] = [
-                (m(K_EXP_GATE, F, d, e), m(K_EXP_UP, F, d, e), m(K_EXP_DOWN, d, F, e))
-                for e in range(s.n_experts)
-            ]
+            L["experts"] = _Experts(
+                lambda e: (m(K_EXP_GATE, F, d, e), m(K_EXP_UP, F, d, e), m(K_EXP_DOWN, d, F, e)),
+                s.n_experts, self.cache_layers)
             L["shared"] = [
                 (m(K_SH_GATE, F, d, e), m(K_SH_UP, F, d, e), m(K_SH_DOWN, d, F, e))
                 for e in range(s.n_shared_experts)

@@ -78,20 +78,21 @@ __global__ void rmsnorm_draft_kernel(const float* __restrict__ x, const bf16_t* 
     rmsnorm_row(x + ((int64_t)b * S + P + i) * d, g, h + (int64_t)r * d, d, eps);
 }
 
-// Merge the per-vocabulary-tile partials of each row.  A workgroup handles 32
-// rows; each of the 8 thread groups of a row takes every 8th
-// tile (online merge in tile order), then the 8 group results are merged in
-// group order through LDS.  The order is fixed, so results are deterministic;
-// ties keep the lower vocabulary id.
+// Merge the per-vocabulary-tile partials of each row.  A workgroup handles 8
+// rows; each of the 32 thread groups of a row takes every 32nd tile (online
+// merge in tile order; one read covers 8 consecutive rows = 128 contiguous
+// bytes), then the 32 group results are merged in group order through LDS.
+// The order is fixed, so results are deterministic; ties keep the lower
+// vocabulary id.
 __global__ __launch_bounds__(256) void lmhead_merge_kernel(const float4* __restrict__ part, int n_tiles, int R,
                                                            int32_t* __restrict__ top1, float* __restrict__ conf,
                                                            float* __restrict__ max_logit) {
-    __shared__ float4 red[8][32];
-    const int rl = threadIdx.x & 31, split = threadIdx.x >> 5;
-    const int r = blockIdx.x * 32 + rl;
+    __shared__ float4 red[32][8];
+    const int rl = threadIdx.x & 7, split = threadIdx.x >> 3;
+    const int r = blockIdx.x * 8 + rl;
     SoftmaxPartial acc{-INFINITY, 0x7fffffff, 0.f};
     if (r < R) {
-        for (int t = split; t < n_tiles; t += 8) {
+        for (int t = split; t < n_tiles; t += 32) {
             const float4 p = part[(int64_t)t * R + r];
             acc = sp_merge(acc, SoftmaxPartial{p.x, __float_as_int(p.y), p.z});
         }
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(256) void lmhead_merge_kernel(const float4* __restr
     __syncthreads();
     if (split == 0 && r < R) {
         SoftmaxPartial a = acc;
-        for (int q = 1; q < 8; ++q) {
+        for (int q = 1; q < 32; ++q) {
             const float4 p = red[q][rl];
             a = sp_merge(a, SoftmaxPartial{p.x, __float_as_int(p.y), p.z});
         }
@@ -206,7 +207,7 @@ void launch_rmsnorm_draft_rows(const float* x, const bf16_t* g, bf16_t* h, int B
 
 void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* top1, float* conf,
                          float* max_logit, hipStream_t st) {
-    hipLaunchKernelGGL(lmhead_merge_kernel, dim3((R + 31) / 32), dim3(256), 0, st, partials,
+    hipLaunchKernelGGL(lmhead_merge_kernel, dim3((R + 7) / 8), dim3(256), 0, st, partials,
                        n_tiles, R, top1, conf, max_logit);
 }
 

@@ -454,3 +454,21 @@ def test_block_wiring_ffn_closed_form():
     y, _ = layer_forward(shape, L, x)
     h = x / np.sqrt(np.mean(x * x, -1, keepdims=True) + shape.norm_eps)
     assert np.allclose(y, x + h * scipy.special.expit(h) * h, rtol=1e-12, atol=1e-13)
+
+
+def test_layer_forward_rows_matches_the_full_block():
+    """The row-subset block (used to check large batches on sampled tokens)
+    equals the full block at those positions, dense and MoE."""
+    from oracle.refine import layer_forward_rows
+    for shape in (MODELS["tiny"].replace(n_layers=1),
+                  MODELS["small_moe"].replace(vocab=96, d_model=64, n_heads=4, n_kv_heads=2, head_dim=16,
+                                              n_experts=6, top_k=2, expert_ffn_dim=16, n_layers=1)):
+        W = oracle.OracleWeights(shape, 5)
+        rng = np.random.default_rng(2)
+        x = rng.standard_normal((2, 19, shape.d_model))
+        full, info = layer_forward(shape, W.layer(0), x)
+        rows = np.array([0, 3, 4, 18])
+        part, pinfo = layer_forward_rows(shape, W.layer(0), x[1], rows)
+        assert np.allclose(part, full[1, rows], rtol=1e-12, atol=1e-12)
+        if shape.n_experts:
+            assert np.array_equal(pinfo["route_ids"], info["route_ids"][1, rows])
