@@ -215,10 +215,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const bool gather = GROUPED && a.a_rows != nullptr;
     buf_rsrc_t a_rsrc, b_rsrc;
     uint32_t a_off[T::A_INSTR], b_off[T::B_INSTR];
-    auto setup_copies = [&](const TileIdx& t) {
-        const bf16_t* Bg = a.B + (GROUPED ? (int64_t)t.g * a.b_group_stride : 0);
+    auto setup_a = [&](const TileIdx& t) {
         a_rsrc = make_rsrc(gather ? a.A : a.A + (int64_t)(t.row_base + t.m0) * a.lda);
-        b_rsrc = make_rsrc(Bg + (int64_t)t.n0 * a.ldb);
 #pragma unroll
         for (int p = 0; p < T::A_INSTR; ++p) {
             const int tr = (wv * T::A_INSTR + p) * RPB + rin;     // row within the tile
@@ -226,6 +224,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             const int64_t grow = gather ? (int64_t)a.a_rows[t.row_base + r] : (int64_t)(r - t.m0);
             a_off[p] = (uint32_t)(grow * a.lda * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
         }
+    };
+    auto setup_b = [&](const TileIdx& t) {
+        const bf16_t* Bg = a.B + (GROUPED ? (int64_t)t.g * a.b_group_stride : 0);
+        b_rsrc = make_rsrc(Bg + (int64_t)t.n0 * a.ldb);
 #pragma unroll
         for (int p = 0; p < T::B_INSTR; ++p) {
             const int tr = (wv * T::B_INSTR + p) * RPB + rin;
@@ -257,7 +259,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
             issue_a(kt_a, st_a);
         }
     };
-    auto prologue = [&](int nk) {                                // first K tiles of a tile
+    auto prologue = [&](int nk) {                                // first K tiles of a tile, stages 0..
 #pragma unroll
         for (int t = 0; t < T::SD; ++t) {
             if constexpr (SA <= SB) {
@@ -331,27 +333,41 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     // past the end of K, into a stage that is never multiplied), which keeps
     // every wait count a compile-time constant.
     const int nk = a.K / BK;
+    // With more K tiles than stages, copies run continuously across tiles:
+    // once a tile's own copies are all issued, the copy slots of its last
+    // iterations fetch the next tile's first K tiles (stage indices carry
+    // over), so a tile switch leaves one round of copies and no drain.
+    // Otherwise every tile starts from a prologue of its own.
+    const bool cont = nk > T::SD;
     TileIdx cur = decode(L);
-    setup_copies(cur);
+    setup_a(cur);
+    setup_b(cur);
     prologue(nk);
+    int sa0 = 0, sb0 = 0;                   // stages of K tile 0 of the current tile
+    bool first = true;
 
     // ---------------------------------------------------------------- per tile
     while (true) {
     const int m0 = cur.m0, rows = cur.rows, row_base = cur.row_base, n0 = cur.n0;
+    const int L_next = L + stride;
+    const bool more = L_next < x_end;
+    const TileIdx nxt = more ? decode(L_next) : cur;
+    const bool flow = cont && more;          // this tile's loop also copies for the next tile
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
 #pragma unroll
         for (int j = 0; j < T::TN; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-    wait_vmcnt<T::N_TOP>();                 // K tile 0 landed, later ones may fly
+    if (first || !cont) wait_vmcnt<T::N_TOP>();   // K tile 0 landed, later ones may fly
+    else wait_vmcnt<T::N_LOOP>();                 // the continuous pipeline's steady-state wait
     __syncthreads();
     // In grouped mode the last row tile of a group is often partly empty; a
     // wave whose rows all lie past the group's end skips its MFMAs (and
     // fragment reads) but still copies and meets every barrier.
     auto run = [&](auto active) {
         constexpr bool ACTIVE = decltype(active)::value;
-        set_stage(0, 0);
+        set_stage(sa0, sb0);
         if constexpr (ACTIVE) {
 #pragma unroll
             for (int ks = 0; ks < T::KS; ++ks) read_slot(ks);
@@ -360,16 +376,34 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         }
         sched_fence();
 
-        int sa = 0, sb = 0;                     // stages of tile kt
+        int sa = sa0, sb = sb0;                 // stages of K tile kt
         for (int kt = 0; kt < nk - 1; ++kt) {
             const int na = sa + 1 == SA ? 0 : sa + 1, nb = sb + 1 == SB ? 0 : sb + 1;
             wait_vmcnt<T::N_LOOP>();                                // own copies of tile kt+1 landed
             __syncthreads();
             set_stage(na, nb);
+            // Copies of K tiles kt+SA / kt+SB: past the end they belong to the
+            // next tile, whose offsets replace this tile's once its last own
+            // copy is out (set up here, where fragment slots 0 .. PRE-1 are free).
+            int ka = kt + SA, kb = kt + SB;
+            if (flow) {
+                // The indices pass through an empty asm so that the offset
+                // arithmetic is done here, not hoisted out of the K loop (where
+                // its registers would stay live for the whole tile).
+                TileIdx t = nxt;
+                asm volatile("" : "+s"(t.g), "+s"(t.m0), "+s"(t.row_base), "+s"(t.rows), "+s"(t.n0));
+                if (ka == nk) setup_a(t);
+                if (kb == nk) setup_b(t);
+                if (ka >= nk) ka -= nk;
+                if (kb >= nk) kb -= nk;
+            } else {
+                ka = min(ka, nk - 1);
+                kb = min(kb, nk - 1);
+            }
             sched_fence();
-            // step PRE | copies of tiles kt+SA / kt+SB | reads of slots 0 .. PRE-1 of tile kt+1
+            // step PRE | the copies | reads of slots 0 .. PRE-1 of tile kt+1
             if constexpr (ACTIVE) mfmas(PRE);
-            issue(min(kt + SA, nk - 1), sa, min(kt + SB, nk - 1), sb);
+            issue(ka, sa, kb, sb);
             if constexpr (!ACTIVE) {
                 sa = na;
                 sb = nb;
@@ -422,16 +456,24 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     };
     if (!GROUPED || m0 + wm * T::WM < rows) run(std::true_type());
     else run(std::false_type());
-    // Every wave is done with this tile's LDS and no copy of it is in flight:
-    // the next tile's first K tiles are copied while this tile's epilogue runs.
-    wait_all_memory();
-    __syncthreads();
-    const int L_next = L + stride;
-    const bool more = L_next < x_end;
-    if (more) {
-        cur = decode(L_next);
-        setup_copies(cur);
-        prologue(nk);
+    if (flow) {
+        // Every wave is done reading K tile nk-1: its stages take the last
+        // round of the next tile's first copies (A tile SA-1, B tile SB-1).
+        __syncthreads();
+        issue(SA - 1, (sa0 + nk - 1) % SA, SB - 1, (sb0 + nk - 1) % SB);
+        sa0 = (sa0 + nk) % SA;
+        sb0 = (sb0 + nk) % SB;
+    } else {
+        // No copy may still be in flight into LDS when the workgroup moves on
+        // (or ends); the next tile, if any, starts from its own prologue.
+        wait_all_memory();
+        __syncthreads();
+        if (more) {
+            setup_a(nxt);
+            setup_b(nxt);
+            prologue(nk);
+            sa0 = sb0 = 0;
+        }
     }
 
     // ---------------------------------------------------------------- epilogues
@@ -594,7 +636,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         }
     }
     if (!more) break;
+    cur = nxt;
     L = L_next;
+    first = false;
     }
 }
 
