@@ -115,9 +115,34 @@ __device__ __forceinline__ void sched_group() {
 }
 
 // Scheduling fence: the compiler moves no instruction across it.
+// Load of an int that no thread writes during the kernel, through the
+// constant address space: with a wave-uniform address it becomes a scalar
+// load (counted by lgkmcnt, not behind the vector-memory queue).
+__device__ __forceinline__ int ld_const(const int* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return *(const __attribute__((address_space(4))) int*)p;
+#else
+    return *p;
+#endif
+}
+
 __device__ __forceinline__ void sched_fence() {
 #if defined(__HIP_DEVICE_COMPILE__)
     __builtin_amdgcn_sched_barrier(0);
+#endif
+}
+
+// Workgroup barrier without the memory-model fence of __syncthreads (whose
+// release half also waits for every copy into LDS still in flight): it only
+// makes this wave's LDS reads complete first.  Copies that other waves will
+// read must be awaited by count before it; the empty asm statements keep the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 #endif
 }
 

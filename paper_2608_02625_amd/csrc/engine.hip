@@ -342,8 +342,8 @@ dlm_status run_layer(Ctx& x, int l) {
         a.n_kv = KV;
         a.head_dim = hd;
         const int64_t big_tiles = (int64_t)((N + 255) / 256) * ((x.T + 255) / 256);
-        a.variant = big_tiles >= 192 ? 2 : 0;
-        TRY(gemm(x, "gemm_qkv", a, EPI_QKV, false, 256, a.variant == 2 ? 256 : 128, 0));
+        a.variant = big_tiles >= 192 ? 11 : 0;          // ping-pong 8-wave 256x256 tiles
+        TRY(gemm(x, "gemm_qkv", a, EPI_QKV, false, 256, a.variant != 0 ? 256 : 128, 0));
     }
     {
         prof_begin(x, "attention");
@@ -356,9 +356,9 @@ dlm_status run_layer(Ctx& x, int l) {
         a.out = xs;
         a.ldo = d;
         const int64_t big_tiles = (int64_t)((x.T + 255) / 256) * ((d + 255) / 256);
-        a.variant = big_tiles >= 128 ? 2 : 0;
-        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, a.variant == 2 || x.T >= 4096 ? 256 : 128,
-                 a.variant == 2 ? 256 : 128, 0));
+        a.variant = big_tiles >= 128 ? 11 : 0;
+        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, a.variant != 0 || x.T >= 4096 ? 256 : 128,
+                 a.variant != 0 ? 256 : 128, 0));
     }
     LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g2), h, x.T, d, c.norm_eps, x.st));
     if (c.n_experts == 0) {
@@ -405,7 +405,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = a_rows;
         a.out = hexp;
         a.ldo = F;
-        a.variant = 5;                                  // third stage for the streamed expert weights (B)
+        a.variant = 11;                                 // ping-pong, third stage for the streamed expert weights (B)
         TRY(gemm(x, "gemm_expert_gate_up", a, EPI_SWIGLU, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     {
@@ -417,7 +417,7 @@ dlm_status run_layer(Ctx& x, int l) {
         a.a_rows = nullptr;
         a.out = y;
         a.ldo = d;
-        a.variant = 2;
+        a.variant = 11;
         TRY(gemm(x, "gemm_expert_down", a, EPI_BF16, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
     LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d, x.st));
@@ -441,7 +441,7 @@ dlm_status run_head(Ctx& x, int32_t* top1, float* conf, float* maxlogit, float* 
     GemmArgs a = gemm_args(x.wt(x.m->plan.lm), c.d_model, hfin, c.d_model, c.vocab, x.R, c.d_model);
     a.partials = x.at<float4>(x.w.partials);
     a.group_m = 4;
-    a.variant = 6;                                      // third stage for the streamed vocabulary rows (A)
+    a.variant = 12;                                     // ping-pong, third stage for the streamed vocabulary rows (A)
     TRY(gemm(x, "gemm_lm_head", a, EPI_LMHEAD, false, kHeadBM, kHeadBN, 0));
     LAUNCH(x, "lmhead_merge", launch_lmhead_merge(a.partials, x.w.n_vtiles, x.R, top1, conf, maxlogit, x.st));
     if (logits_out) {

@@ -5,7 +5,10 @@
 // grid (two per SIMD), each wave a grid of 32x32 accumulators fed by
 // v_mfma_f32_32x32x16_bf16.  K advances BK at a time through LDS stages filled
 // straight from global memory by buffer loads (no register staging) while the
-// MFMAs of earlier K tiles run.
+// MFMAs of earlier K tiles run.  Two schedules: every wave interleaves its
+// fragment reads with its MFMAs, or (ping-pong, 8 waves) the two waves of a
+// SIMD take turns, one multiplying a whole K tile while the other copies and
+// reads the next.
 // LDS rows are BK*2 bytes with 16-byte chunks XOR-swizzled by row bits so that
 // fragment reads of 32 consecutive rows spread over all banks.
 //
@@ -141,7 +144,7 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
     }
 }
 
-template <int BM, int BN, int BK, int SA, int SB, int NW, int EPI, bool GROUPED>
+template <int BM, int BN, int BK, int SA, int SB, int NW, int EPI, bool GROUPED, bool PP>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void gemm_kernel(GemmArgs a) {
     using T = TileCfg<BM, BN, BK, SA, SB, NW>;
     __shared__ __attribute__((aligned(16))) char smem[T::LDS];
@@ -182,11 +185,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         }
         TileIdx t;
         if (GROUPED) {
-            const int2 e = a.tile_tab[ti];
-            t.g = uniform(e.x);
-            t.m0 = uniform(e.y);
-            t.row_base = uniform(a.grp_off[t.g]);
-            t.rows = uniform(a.grp_off[t.g + 1]) - t.row_base;
+            // The tile table and group offsets are read-only for the whole
+            // launch: scalar loads, no wait behind copies in flight.
+            const int* tab = reinterpret_cast<const int*>(a.tile_tab) + 2 * ti;
+            t.g = uniform(ld_const(tab));
+            t.m0 = uniform(ld_const(tab + 1));
+            t.row_base = uniform(ld_const(a.grp_off + t.g));
+            t.rows = uniform(ld_const(a.grp_off + t.g + 1)) - t.row_base;
         } else {
             t.g = 0;
             t.m0 = ti * BM;
@@ -315,6 +320,172 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     constexpr int NR = T::TM + T::TN, NM = T::TM * T::TN;
     constexpr int PRE = T::KS / 2;          // fragment steps of a tile run before its barrier
 
+    // ---------------------------------------------------------------- epilogues
+    auto epilogue = [&](const int m0, const int rows, const int row_base, const int n0) __attribute__((always_inline)) {
+        // TACC: acc[i][j][4q + r] holds C[row][col] with
+        //   row = wm*WM + i*32 + lane%32,  col = wn*WN + j*32 + 8q + 4*(lane/32) + r.
+        // otherwise acc[i][j][e] holds C[row][col] with
+        //   row = wm*WM + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = wn*WN + j*32 + lane%32.
+        // Lane terms from an opaque copy of the lane id: computed here, not
+        // hoisted out of the tile loop into registers live across the K loop.
+        int lane = threadIdx.x & 63;
+        asm volatile("" : "+v"(lane));
+        const int lrow0 = wm * T::WM + 4 * (lane >> 5);
+        const int lcol0 = wn * T::WN + (lane & 31);
+        const int trow = m0 + wm * T::WM + (lane & 31);              // TACC row of block i = 0
+        const int tcol = n0 + wn * T::WN + 4 * (lane >> 5);          // TACC column of j = 0, q = 0
+        // 4-column groups are stored whole when they lie inside N and rows are
+        // 16-byte (f32) / 8-byte (bf16) aligned.
+        const bool vec = (a.ldo & 3) == 0;
+        const bool full_tile = m0 + BM <= rows && n0 + BN <= a.N;
+
+        if constexpr (EPI == EPI_RESID) {
+            // out[row][col] += acc: per 32-row block all 16 x TN loads are issued
+            // before the adds and stores.
+            float* out = reinterpret_cast<float*>(a.out);
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+                float old[16][T::TN];
+                const int rb = m0 + lrow0 + i * 32;
+                if (full_tile) {
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+#pragma unroll
+                        for (int j = 0; j < T::TN; ++j)
+                            old[e][j] = out[(int64_t)(rb + 8 * (e >> 2) + (e & 3)) * a.ldo + n0 + lcol0 + j * 32];
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+#pragma unroll
+                        for (int j = 0; j < T::TN; ++j)
+                            out[(int64_t)(rb + 8 * (e >> 2) + (e & 3)) * a.ldo + n0 + lcol0 + j * 32] =
+                                old[e][j] + acc[i][j][e];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+#pragma unroll
+                        for (int j = 0; j < T::TN; ++j) {
+                            const int r = rb + 8 * (e >> 2) + (e & 3), c = n0 + lcol0 + j * 32;
+                            old[e][j] = (r < rows && c < a.N) ? out[(int64_t)r * a.ldo + c] : 0.f;
+                        }
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+#pragma unroll
+                        for (int j = 0; j < T::TN; ++j) {
+                            const int r = rb + 8 * (e >> 2) + (e & 3), c = n0 + lcol0 + j * 32;
+                            if (r < rows && c < a.N) out[(int64_t)r * a.ldo + c] = old[e][j] + acc[i][j][e];
+                        }
+                }
+            }
+        } else if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_T) {
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int rl = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                    if (rl >= rows) continue;
+                    const int64_t orow = GROUPED ? (int64_t)row_base + rl : rl;
+#pragma unroll
+                    for (int j = 0; j < T::TN; ++j) {
+                        const int c = n0 + lcol0 + j * 32;
+                        if (c >= a.N) continue;
+                        const float v = acc[i][j][e];
+                        if constexpr (EPI == EPI_BF16)
+                            reinterpret_cast<bf16_t*>(a.out)[orow * a.ldo + c] = f32_to_bf16(v);
+                        else if constexpr (EPI == EPI_F32)
+                            reinterpret_cast<float*>(a.out)[orow * a.ldo + c] = v;
+                        else
+                            reinterpret_cast<float*>(a.out)[(int64_t)c * a.ldo + orow] = v;
+                    }
+                }
+        } else if constexpr (EPI == EPI_SWIGLU) {
+            // Physical columns alternate 32 gate / 32 up: blocks (j, j+1) hold the
+            // gate and up values of the same 32 features; 4 consecutive features
+            // per lane leave as one 8-byte store.
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+                const int r = trow + i * 32;
+                if (r >= rows) continue;
+                bf16_t* orow = reinterpret_cast<bf16_t*>(a.out) + (GROUPED ? (int64_t)row_base + r : r) * a.ldo;
+#pragma unroll
+                for (int j = 0; j < T::TN; j += 2) {
+                    const int c0 = n0 + wn * T::WN + j * 32;                // first gate column of the pair
+                    if (c0 >= a.N) continue;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        float hv[4];
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const float gt = acc[i][j][4 * q + t], up = acc[i][j + 1][4 * q + t];
+                            hv[t] = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
+                        }
+                        const int f = (c0 >> 1) + 8 * q + 4 * (lane >> 5);
+                        if (vec)
+                            *reinterpret_cast<u32x2*>(orow + f) = u32x2{pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
+                        else {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) orow[f + t] = f32_to_bf16(hv[t]);
+                        }
+                    }
+                }
+            }
+        } else if constexpr (EPI == EPI_QKV) {
+            static_assert(T::WM % 128 == 0, "a wave's rows must cover whole heads");
+            if (a.head_dim == 128)
+                qkv_epilogue<T::TM, T::TN, 128>(a, acc, m0, n0, lrow0, lcol0);
+            else
+                qkv_epilogue<T::TM, T::TN, 64>(a, acc, m0, n0, lrow0, lcol0);
+        } else if constexpr (EPI == EPI_LMHEAD) {
+            // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
+            // sum exp(z - max)) over each half tile's BM/2 vocabulary rows.
+            SoftmaxPartial part[T::TN];
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j) {
+                float m = -INFINITY;
+                int idx = 0x7fffffff;
+#pragma unroll
+                for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                        const float z = (v < rows) ? acc[i][j][e] : -INFINITY;
+                        if (z > m) {
+                            m = z;
+                            idx = v;
+                        }
+                    }
+                float s = 0.f;
+                if (m != -INFINITY) {
+                    const float ml = m * kLog2e;
+#pragma unroll
+                    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) {
+                            const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                            if (v < rows) s += exp2f(acc[i][j][e] * kLog2e - ml);
+                        }
+                }
+                SoftmaxPartial p{m, idx, s};
+                SoftmaxPartial q;
+                q.m = __shfl_xor(p.m, 32, 64);
+                q.idx = __shfl_xor(p.idx, 32, 64);
+                q.s = __shfl_xor(p.s, 32, 64);
+                part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
+            }
+            // One partial per (BM/2-row half tile, token): the two wave rows
+            // (wm = 0, 1) write separately and the merge kernel combines them.
+            if (lane < 32) {
+                const int half = (m0 / BM) * 2 + wm;
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j) {
+                    const int c = n0 + lcol0 + j * 32;
+                    if (c < a.N)
+                        a.partials[(int64_t)half * a.N + c] =
+                            make_float4(part[j].m, __int_as_float(part[j].idx), part[j].s, 0.f);
+                }
+            }
+        }
+    };
+
     // Software pipeline over K tiles (A of tile kt lives in A stage kt % SA,
     // B in B stage kt % SB;
     // registers hold every fragment of the tile being multiplied).  Per tile,
@@ -339,6 +510,199 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     // over), so a tile switch leaves one round of copies and no drain.
     // Otherwise every tile starts from a prologue of its own.
     const bool cont = nk > T::SD;
+    if constexpr (PP) {
+        // Ping-pong schedule (8 waves, two per SIMD).  Waves 0-3 (group 0, the
+        // first BM/2 rows of the tile) and waves 4-7 (group 1, the other half)
+        // alternate between a compute phase (all MFMAs of one K tile and nothing
+        // else) and a memory phase (one round of copies into LDS, then every
+        // fragment of the next K tile read into registers); a workgroup barrier
+        // ends each phase.  While one wave of a SIMD multiplies, the other loads,
+        // so the matrix core is never left waiting on LDS or on the other wave.
+        // K tile k is read by group 0 in phase 2k and by group 1 in phase 2k+1,
+        // so its stages are free from phase 2k+2 on.  Group 0 copies the operand
+        // with fewer stages (S = 2: issued in phase 2k+2 for K tile k+S, awaited
+        // at the end of phase 2(k+S)-1), group 1 the one with more (S = 3: issued
+        // in phase 2k+3, awaited at the end of its memory phase 2(k+S)-1).  In
+        // both cases S-2 later rounds of the same wave may still be in flight at
+        // the wait.  Output tiles follow each other without a drain (as in the
+        // other schedule): a group stores a finished tile at the start of its
+        // next memory phase.
+        static_assert(NW == 8 && T::SS == 2 && T::SD == 3, "ping-pong: 8 waves, 2 + 3 stages");
+        auto group = [&](auto gc) __attribute__((always_inline)) {
+            constexpr int G = decltype(gc)::value;
+            constexpr int S = G == 0 ? T::SS : T::SD;                // stages of the operand this group copies
+            constexpr bool CA = (G == 0) == (SA <= SB);               // this group copies A (else B)
+            constexpr int OP_BYTES = CA ? T::A_BYTES : T::B_BYTES;
+            constexpr int NI = OP_BYTES / 1024 / (NW / 2);             // 1 KB copy blocks per wave and K tile
+            constexpr int OP_BASE = CA ? 0 : B_BASE;
+            const int gw = wn;                                          // wave within the group
+            buf_rsrc_t rsrc;
+            uint32_t off[NI];
+            auto setup = [&](const TileIdx& t) __attribute__((always_inline)) {
+                // Lane terms recomputed from an opaque copy of the lane id, so
+                // that they are not kept live across the K loop.
+                int ln = lane;
+                asm volatile("" : "+v"(ln));
+                const int rin = ln / CPR, pc = ln % CPR;
+                if constexpr (CA) {
+                    rsrc = make_rsrc(gather ? a.A : a.A + (int64_t)(t.row_base + t.m0) * a.lda);
+#pragma unroll
+                    for (int p = 0; p < NI; ++p) {
+                        const int tr = (gw * NI + p) * RPB + rin;
+                        const int r = min(t.m0 + tr, t.rows - 1);
+                        const int64_t grow = gather ? (int64_t)a.a_rows[t.row_base + r] : (int64_t)(r - t.m0);
+                        off[p] = (uint32_t)(grow * a.lda * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
+                    }
+                } else {
+                    const bf16_t* Bg = a.B + (GROUPED ? (int64_t)t.g * a.b_group_stride : 0);
+                    rsrc = make_rsrc(Bg + (int64_t)t.n0 * a.ldb);
+#pragma unroll
+                    for (int p = 0; p < NI; ++p) {
+                        const int tr = (gw * NI + p) * RPB + rin;
+                        const int n = min(t.n0 + tr, a.N - 1) - t.n0;
+                        off[p] = (uint32_t)((int64_t)n * a.ldb * 2) + (uint32_t)((pc ^ swz_key<CPR>(tr)) * 16);
+                    }
+                }
+            };
+            auto copy = [&](int kt, int stage) {                       // this group's part of K tile kt
+                const int dst = OP_BASE + stage * OP_BYTES + gw * NI * 1024;
+#pragma unroll
+                for (int p = 0; p < NI; ++p) lds_dma16_buf(rsrc, off[p], kt * (BK * 2), lds_at(dst + p * 1024));
+            };
+            auto start = [&](const TileIdx& t) {                       // K tiles 0 .. S-1 into stages 0 .. S-1
+                setup(t);
+#pragma unroll
+                for (int s = 0; s < S; ++s) copy(min(s, nk - 1), s);
+            };
+            // All MFMAs of one K tile.  The first K tile of an output tile
+            // starts from a zero accumulator (an inline-constant operand), so
+            // the accumulators are never cleared separately; it is multiplied
+            // even by a wave with no rows in the tile, which keeps no older
+            // accumulator live.
+            auto compute = [&](auto first_tag) __attribute__((always_inline)) {
+                constexpr bool FIRST = decltype(first_tag)::value;
+#pragma unroll
+                for (int ks = 0; ks < T::KS; ++ks)
+#pragma unroll
+                    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < T::TN; ++j) {
+                            const f32x16 c = (FIRST && ks == 0) ? f32x16{} : acc[i][j];
+                            acc[i][j] = TACC ? mfma32x32x16(rb[ks][j], ra[ks][i], c)
+                                             : mfma32x32x16(ra[ks][i], rb[ks][j], c);
+                        }
+            };
+            // A wave whose rows all lie past the end of a grouped tile's rows
+            // skips its MFMAs but still copies, reads and meets every barrier.
+            auto active = [&](const TileIdx& t) { return !GROUPED || t.m0 + wm * T::WM < t.rows; };
+
+            TileIdx cur = decode(L), prv = cur;
+            bool act = active(cur);
+            bool pend = false;                  // tile prv awaits its epilogue (stored in K step 0)
+            int sa = 0, sb = 0;                 // stages of the next K tile to read
+            bool fresh = true;                  // the current tile began with a prologue
+            start(cur);
+            wait_vmcnt<NI * (S - 1)>();         // own part of K tile 0 landed
+            lds_barrier();
+            if constexpr (G == 1) lds_barrier();     // phase 0: group 0 reads, group 1 waits
+            while (true) {
+                const int L_next = L + stride;
+                const bool more = L_next < x_end;
+                const TileIdx nxt = more ? decode(L_next) : cur;
+                const bool flow = cont && more;
+                // One K tile: copy local K tile x (x < 0: none) into the stage
+                // of K tile kt-1, read K tile kt, barrier, multiply, barrier.
+                // K step 0 of a tile that follows another without a drain also
+                // stores that tile in its memory phase: a store-only epilogue
+                // after the copy (and, for group 1, after its wait, so that the
+                // stores are newer than every copy awaited before the next
+                // phase), one that also loads before the copy.
+                constexpr bool EPI_LOADS = EPI == EPI_RESID || EPI == EPI_QKV;
+                auto step = [&](int kt, int x, auto first_tag) __attribute__((always_inline)) {
+                    constexpr bool FIRST = decltype(first_tag)::value;
+                    // ---- memory phase
+                    const int so = CA ? sa : sb;                        // own stage of K tile kt
+                    bool waited = false;
+                    if constexpr (FIRST && EPI_LOADS) {
+                        // An epilogue that loads must not wait behind this
+                        // phase's copies: it runs before them.
+                        if (pend) {
+                            epilogue(prv.m0, prv.rows, prv.row_base, prv.n0);
+                            sched_fence();
+                            pend = false;
+                        }
+                    }
+                    if (x >= 0) copy(x, so == 0 ? S - 1 : so - 1);
+                    if constexpr (FIRST && !EPI_LOADS) {
+                        if (pend) {
+                            if constexpr (G == 1) wait_vmcnt<NI * (S - 2)>();   // own part of K tile 1 landed
+                            sched_fence();
+                            epilogue(prv.m0, prv.rows, prv.row_base, prv.n0);
+                            sched_fence();
+                            pend = false;
+                            waited = true;
+                        }
+                    }
+                    set_stage(sa, sb);
+#pragma unroll
+                    for (int ks = 0; ks < T::KS; ++ks) read_slot(ks);
+                    sa = sa + 1 == SA ? 0 : sa + 1;
+                    sb = sb + 1 == SB ? 0 : sb + 1;
+                    if constexpr (G == 1) {
+                        if (!waited) wait_vmcnt<NI * (S - 2)>();        // own part of K tile kt+1 landed
+                    }
+                    sched_fence();
+                    lds_barrier();
+                    // ---- compute phase
+                    if (FIRST || act) compute(first_tag);
+                    sched_fence();
+                    if constexpr (G == 0) wait_vmcnt<NI * (S - 2)>();   // own part of K tile kt+1 landed
+                    lds_barrier();
+                    sched_fence();
+                };
+                // Copies issued in K step kt fetch K tile kt-1+S.  With
+                // continuous copies, those past the end fetch the next tile's
+                // first K tiles (its offsets are set up between the two loops);
+                // otherwise they repeat the last K tile into a stage that is
+                // never read, which keeps every wait count constant.
+                const int kt_sw = flow ? nk + 1 - S : nk;
+                step(0, fresh ? -1 : min(S - 1, nk - 1), std::true_type());
+                for (int kt = 1; kt < kt_sw; ++kt) step(kt, min(kt - 1 + S, nk - 1), std::false_type());
+                if (flow) {
+                    setup(nxt);
+#pragma unroll
+                    for (int c = 0; c < S - 1; ++c) step(kt_sw + c, c, std::false_type());
+                    prv = cur;
+                    pend = true;
+                    cur = nxt;
+                    L = L_next;
+                    act = active(cur);
+                    fresh = false;
+                    continue;
+                }
+                // Drain: group 0 stores while group 1 multiplies its last K
+                // tile (one more barrier for group 0), then group 1 stores.
+                epilogue(cur.m0, cur.rows, cur.row_base, cur.n0);
+                if constexpr (G == 0) __syncthreads();
+                if (!more) break;
+                // Short K (no continuous copies): every copy lands before the
+                // next tile's prologue refills the stages.
+                wait_all_memory();
+                __syncthreads();
+                cur = nxt;
+                L = L_next;
+                act = active(cur);
+                sa = sb = 0;
+                fresh = true;
+                start(cur);
+                wait_vmcnt<NI * (S - 1)>();
+                lds_barrier();
+                if constexpr (G == 1) lds_barrier();
+            }
+        };
+        if (wm == 0) group(std::integral_constant<int, 0>());
+        else group(std::integral_constant<int, 1>());
+    } else {
     TileIdx cur = decode(L);
     setup_a(cur);
     setup_b(cur);
@@ -476,178 +840,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         }
     }
 
-    // ---------------------------------------------------------------- epilogues
-    // TACC: acc[i][j][4q + r] holds C[row][col] with
-    //   row = wm*WM + i*32 + lane%32,  col = wn*WN + j*32 + 8q + 4*(lane/32) + r.
-    // otherwise acc[i][j][e] holds C[row][col] with
-    //   row = wm*WM + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = wn*WN + j*32 + lane%32.
-    const int lrow0 = wm * T::WM + 4 * (lane >> 5);
-    const int lcol0 = wn * T::WN + (lane & 31);
-    const int trow = m0 + wm * T::WM + (lane & 31);              // TACC row of block i = 0
-    const int tcol = n0 + wn * T::WN + 4 * (lane >> 5);          // TACC column of j = 0, q = 0
-    // 4-column groups are stored whole when they lie inside N and rows are
-    // 16-byte (f32) / 8-byte (bf16) aligned.
-    const bool vec = (a.ldo & 3) == 0;
-    const bool full_tile = m0 + BM <= rows && n0 + BN <= a.N;
-
-    if constexpr (EPI == EPI_RESID) {
-        // out[row][col] += acc: per 32-row block all 16 x TN loads are issued
-        // before the adds and stores.
-        float* out = reinterpret_cast<float*>(a.out);
-#pragma unroll
-        for (int i = 0; i < T::TM; ++i) {
-            float old[16][T::TN];
-            const int rb = m0 + lrow0 + i * 32;
-            if (full_tile) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-#pragma unroll
-                    for (int j = 0; j < T::TN; ++j)
-                        old[e][j] = out[(int64_t)(rb + 8 * (e >> 2) + (e & 3)) * a.ldo + n0 + lcol0 + j * 32];
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-#pragma unroll
-                    for (int j = 0; j < T::TN; ++j)
-                        out[(int64_t)(rb + 8 * (e >> 2) + (e & 3)) * a.ldo + n0 + lcol0 + j * 32] =
-                            old[e][j] + acc[i][j][e];
-            } else {
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-#pragma unroll
-                    for (int j = 0; j < T::TN; ++j) {
-                        const int r = rb + 8 * (e >> 2) + (e & 3), c = n0 + lcol0 + j * 32;
-                        old[e][j] = (r < rows && c < a.N) ? out[(int64_t)r * a.ldo + c] : 0.f;
-                    }
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-#pragma unroll
-                    for (int j = 0; j < T::TN; ++j) {
-                        const int r = rb + 8 * (e >> 2) + (e & 3), c = n0 + lcol0 + j * 32;
-                        if (r < rows && c < a.N) out[(int64_t)r * a.ldo + c] = old[e][j] + acc[i][j][e];
-                    }
-            }
-        }
-    } else if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_T) {
-#pragma unroll
-        for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int rl = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-                if (rl >= rows) continue;
-                const int64_t orow = GROUPED ? (int64_t)row_base + rl : rl;
-#pragma unroll
-                for (int j = 0; j < T::TN; ++j) {
-                    const int c = n0 + lcol0 + j * 32;
-                    if (c >= a.N) continue;
-                    const float v = acc[i][j][e];
-                    if constexpr (EPI == EPI_BF16)
-                        reinterpret_cast<bf16_t*>(a.out)[orow * a.ldo + c] = f32_to_bf16(v);
-                    else if constexpr (EPI == EPI_F32)
-                        reinterpret_cast<float*>(a.out)[orow * a.ldo + c] = v;
-                    else
-                        reinterpret_cast<float*>(a.out)[(int64_t)c * a.ldo + orow] = v;
-                }
-            }
-    } else if constexpr (EPI == EPI_SWIGLU) {
-        // Physical columns alternate 32 gate / 32 up: blocks (j, j+1) hold the
-        // gate and up values of the same 32 features; 4 consecutive features
-        // per lane leave as one 8-byte store.
-#pragma unroll
-        for (int i = 0; i < T::TM; ++i) {
-            const int r = trow + i * 32;
-            if (r >= rows) continue;
-            bf16_t* orow = reinterpret_cast<bf16_t*>(a.out) + (GROUPED ? (int64_t)row_base + r : r) * a.ldo;
-#pragma unroll
-            for (int j = 0; j < T::TN; j += 2) {
-                const int c0 = n0 + wn * T::WN + j * 32;                // first gate column of the pair
-                if (c0 >= a.N) continue;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float hv[4];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const float gt = acc[i][j][4 * q + t], up = acc[i][j + 1][4 * q + t];
-                        hv[t] = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
-                    }
-                    const int f = (c0 >> 1) + 8 * q + 4 * (lane >> 5);
-                    if (vec)
-                        *reinterpret_cast<u32x2*>(orow + f) = u32x2{pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
-                    else {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) orow[f + t] = f32_to_bf16(hv[t]);
-                    }
-                }
-            }
-        }
-    } else if constexpr (EPI == EPI_QKV) {
-        static_assert(T::WM % 128 == 0, "a wave's rows must cover whole heads");
-        if (a.head_dim == 128)
-            qkv_epilogue<T::TM, T::TN, 128>(a, acc, m0, n0, lrow0, lcol0);
-        else
-            qkv_epilogue<T::TM, T::TN, 64>(a, acc, m0, n0, lrow0, lcol0);
-    } else if constexpr (EPI == EPI_LMHEAD) {
-        // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
-        // sum exp(z - max)) over each half tile's BM/2 vocabulary rows.
-        SoftmaxPartial part[T::TN];
-#pragma unroll
-        for (int j = 0; j < T::TN; ++j) {
-            float m = -INFINITY;
-            int idx = 0x7fffffff;
-#pragma unroll
-            for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-                    const float z = (v < rows) ? acc[i][j][e] : -INFINITY;
-                    if (z > m) {
-                        m = z;
-                        idx = v;
-                    }
-                }
-            float s = 0.f;
-            if (m != -INFINITY) {
-                const float ml = m * kLog2e;
-#pragma unroll
-                for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-                        if (v < rows) s += exp2f(acc[i][j][e] * kLog2e - ml);
-                    }
-            }
-            SoftmaxPartial p{m, idx, s};
-            SoftmaxPartial q;
-            q.m = __shfl_xor(p.m, 32, 64);
-            q.idx = __shfl_xor(p.idx, 32, 64);
-            q.s = __shfl_xor(p.s, 32, 64);
-            part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
-        }
-        // One partial per (BM/2-row half tile, token): the two wave rows
-        // (wm = 0, 1) write separately and the merge kernel combines them.
-        if (lane < 32) {
-            const int half = (m0 / BM) * 2 + wm;
-#pragma unroll
-            for (int j = 0; j < T::TN; ++j) {
-                const int c = n0 + lcol0 + j * 32;
-                if (c < a.N)
-                    a.partials[(int64_t)half * a.N + c] =
-                        make_float4(part[j].m, __int_as_float(part[j].idx), part[j].s, 0.f);
-            }
-        }
-    }
+    epilogue(m0, rows, row_base, n0);
     if (!more) break;
     cur = nxt;
     L = L_next;
     first = false;
     }
+    }
 }
 
-template <int BM, int BN, int BK, int SA, int SB, int NW, int EPI, bool GROUPED>
+template <int BM, int BN, int BK, int SA, int SB, int NW, int EPI, bool GROUPED, bool PP>
 hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     if constexpr (EPI == EPI_QKV && (BM / 2) % 128 != 0) {
         return hipErrorInvalidValue;                       // RoPE pairs must stay inside one wave
     } else {
-    auto kernel = gemm_kernel<BM, BN, BK, SA, SB, NW, EPI, GROUPED>;
+    auto kernel = gemm_kernel<BM, BN, BK, SA, SB, NW, EPI, GROUPED, PP>;
     // Workgroups that fit on the device at once (a multiple of 8, one share
     // per XCD); a persistent grid of at most that many walks all tiles.
     static int resident = 0;
@@ -674,27 +881,30 @@ hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
 // variant 0: 4 waves; 1: alternative stage/BK choices; 2: 8 waves, 2+2
 // stages; 5: 8 waves with a third B stage (B streamed from far memory, e.g.
 // expert weights); 6: 8 waves with a third A stage (A streamed, e.g. the LM
-// head's vocabulary rows).  The 256x256 8-wave tiles with a third stage use
-// all 160 KB of LDS.
+// head's vocabulary rows); 11 / 12: as 5 / 6 with the ping-pong schedule (the
+// two waves of a SIMD alternate between multiplying and loading).  The
+// 256x256 8-wave tiles with a third stage use all 160 KB of LDS.
 template <int EPI, bool GROUPED>
 hipError_t launch_tiles(const GemmArgs& a, int bm, int bn, int max_tiles, hipStream_t st) {
     if (a.variant == 1) {
-        if (bm == 256 && bn == 256) return launch_t<256, 256, 32, 4, 4, 4, EPI, GROUPED>(a, max_tiles, st);
-        if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 3, 3, 4, EPI, GROUPED>(a, max_tiles, st);
-        if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+        if (bm == 256 && bn == 256) return launch_t<256, 256, 32, 4, 4, 4, EPI, GROUPED, false>(a, max_tiles, st);
+        if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 3, 3, 4, EPI, GROUPED, false>(a, max_tiles, st);
+        if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 2, 2, 4, EPI, GROUPED, false>(a, max_tiles, st);
         return hipErrorInvalidValue;
     }
     if (bm == 256 && bn == 256) {
-        if (a.variant == 2) return launch_t<256, 256, 64, 2, 2, 8, EPI, GROUPED>(a, max_tiles, st);
-        if (a.variant == 5) return launch_t<256, 256, 64, 2, 3, 8, EPI, GROUPED>(a, max_tiles, st);
-        if (a.variant == 6) return launch_t<256, 256, 64, 3, 2, 8, EPI, GROUPED>(a, max_tiles, st);
+        if (a.variant == 2) return launch_t<256, 256, 64, 2, 2, 8, EPI, GROUPED, false>(a, max_tiles, st);
+        if (a.variant == 5) return launch_t<256, 256, 64, 2, 3, 8, EPI, GROUPED, false>(a, max_tiles, st);
+        if (a.variant == 6) return launch_t<256, 256, 64, 3, 2, 8, EPI, GROUPED, false>(a, max_tiles, st);
+        if (a.variant == 11) return launch_t<256, 256, 64, 2, 3, 8, EPI, GROUPED, true>(a, max_tiles, st);
+        if (a.variant == 12) return launch_t<256, 256, 64, 3, 2, 8, EPI, GROUPED, true>(a, max_tiles, st);
     }
     if (a.variant != 0) return hipErrorInvalidValue;
-    if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 3, 3, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 256) return launch_t<128, 256, 64, 3, 3, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
-    if (bm == 128 && bn == 64) return launch_t<128, 64, 64, 2, 2, 4, EPI, GROUPED>(a, max_tiles, st);
+    if (bm == 256 && bn == 256) return launch_t<256, 256, 64, 2, 2, 4, EPI, GROUPED, false>(a, max_tiles, st);
+    if (bm == 256 && bn == 128) return launch_t<256, 128, 64, 3, 3, 4, EPI, GROUPED, false>(a, max_tiles, st);
+    if (bm == 128 && bn == 256) return launch_t<128, 256, 64, 3, 3, 4, EPI, GROUPED, false>(a, max_tiles, st);
+    if (bm == 128 && bn == 128) return launch_t<128, 128, 64, 2, 2, 4, EPI, GROUPED, false>(a, max_tiles, st);
+    if (bm == 128 && bn == 64) return launch_t<128, 64, 64, 2, 2, 4, EPI, GROUPED, false>(a, max_tiles, st);
     return hipErrorInvalidValue;
 }
 

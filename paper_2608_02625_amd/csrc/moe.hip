@@ -87,13 +87,15 @@ __global__ __launch_bounds__(1024) void router_topk_kernel(const bf16_t* __restr
 #pragma unroll
         for (int e = 0; e < 16; ++e) zs[kc][j][(blk0 + b) * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = acc[b][e];
     __syncthreads();
-    // Sum the K parts in a fixed order; logits of experts >= E become -inf.
+    // Sum the K parts in a fixed order; logits of experts >= E become -inf,
+    // and so does a NaN logit, so that the rank order below stays total and
+    // every token receives exactly k distinct experts whatever its input.
     for (int i = threadIdx.x; i < 32 * EP; i += NW * 64) {
         const int tt = i / EP, e = i - tt * EP;
         float z = zs[0][tt][e];
 #pragma unroll
         for (int s = 1; s < KSPLIT; ++s) z += zs[s][tt][e];
-        zs[0][tt][e] = e < E ? z : -INFINITY;
+        zs[0][tt][e] = (e < E && z == z) ? z : -INFINITY;
     }
     __syncthreads();
 

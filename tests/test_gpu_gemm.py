@@ -23,6 +23,17 @@ pytestmark = pytest.mark.gpu
     (600, 520, 640, ((5 << 16) | 256, 256)),
     (777, 300, 1088, ((6 << 16) | 256, 256)),
     (256, 256, 64, ((5 << 16) | 256, 256)),
+    # ping-pong schedule (2 + 3 and 3 + 2 stages): one K tile, short K with a
+    # prologue per tile, continuous copies, and more tiles than resident
+    # workgroups (several output tiles per workgroup) with short and long K
+    (256, 256, 64, ((11 << 16) | 256, 256)),
+    (300, 200, 128, ((11 << 16) | 256, 256)),
+    (600, 520, 640, ((11 << 16) | 256, 256)),
+    (777, 300, 1088, ((12 << 16) | 256, 256)),
+    (1, 1, 64, ((12 << 16) | 256, 256)),
+    (8229, 2100, 128, ((11 << 16) | 256, 256)),
+    (8229, 2100, 320, ((11 << 16) | 256, 256)),
+    (8229, 2100, 320, ((12 << 16) | 256, 256)),
 ])
 def test_gemm_matches_fp32_reference(m, n, k, tile):
     need_gpu()

@@ -27,13 +27,15 @@ def _functions(path):
 
 def masked_mfmas(lines):
     """MFMAs issued after an EXEC-narrowing s_and_saveexec that is not
-    followed by s_cbranch_execz, before EXEC is restored."""
+    followed by a branch on EXEC being empty (s_cbranch_execz over the region,
+    or s_cbranch_execnz into a region placed out of line), before EXEC is
+    restored."""
     bad, masked = 0, False
     for i, l in enumerate(lines):
         op = l.split()[0]
         if "saveexec" in op:
             nxt = lines[i + 1].split()[0] if i + 1 < len(lines) else ""
-            masked = nxt != "s_cbranch_execz"
+            masked = nxt not in ("s_cbranch_execz", "s_cbranch_execnz")
         elif op.startswith("s_or_b64") and "exec, exec" in l:
             masked = False
         elif op.startswith("v_mfma") and masked:
@@ -46,6 +48,8 @@ def test_scanner_flags_a_masked_mfma():
              "v_mfma_f32_32x32x16_bf16 a[0:15], v[44:47], v[72:75], a[0:15]", "s_or_b64 exec, exec, s[8:9]"]
     assert masked_mfmas(lines) == 1
     lines.insert(2, "s_cbranch_execz .LBB0_3")
+    assert masked_mfmas(lines) == 0
+    lines[2] = "s_cbranch_execnz .LBB0_3"
     assert masked_mfmas(lines) == 0
 
 
