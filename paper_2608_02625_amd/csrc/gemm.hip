@@ -303,12 +303,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         for (int j = 0; j < T::TN; ++j)
             rb[ks][j] = *(lds_frag*)((lds_char*)lds + fb + j * 32 * T::ROW);
     };
-    // The SwiGLU epilogue takes the accumulators transposed (operands
-    // swapped): a lane then holds 4 consecutive output features of one row,
-    // stored as one 8-byte write.  The other epilogues keep rows in the
-    // accumulator's 4-element groups (consecutive lanes = consecutive columns:
-    // fully coalesced 2-row stores).
-    constexpr bool TACC = EPI == EPI_SWIGLU;
+    // The SwiGLU epilogue, and the bf16 one under the ping-pong schedule, take
+    // the accumulators transposed (operands swapped): a lane then holds 4
+    // consecutive output columns of one row, stored as one 8-byte write (a
+    // quarter of the store instructions; under ping-pong the epilogue runs
+    // inside a memory phase, where that count matters).  The other epilogues
+    // keep rows in the accumulator's 4-element groups (consecutive lanes =
+    // consecutive columns: fully coalesced 2-row accesses; measured faster for
+    // the residual read-modify-write).
+    constexpr bool TACC = EPI == EPI_SWIGLU || (PP && EPI == EPI_BF16);
     auto mfmas = [&](int ks) {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
@@ -339,7 +342,30 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         const bool vec = (a.ldo & 3) == 0;
         const bool full_tile = m0 + BM <= rows && n0 + BN <= a.N;
 
-        if constexpr (EPI == EPI_RESID) {
+        if constexpr (EPI == EPI_BF16 && TACC) {
+            // 4 consecutive columns of one row per lane: one 8-byte store.
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+                const int r = trow + i * 32;
+                if (r >= rows) continue;
+                bf16_t* orow = reinterpret_cast<bf16_t*>(a.out) + (GROUPED ? (int64_t)row_base + r : r) * a.ldo;
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int c = tcol + j * 32 + 8 * q;
+                        const float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                            acc[i][j][4 * q + 3]};
+                        if (vec && c + 3 < a.N) {
+                            *reinterpret_cast<u32x2*>(orow + c) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                        } else {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t)
+                                if (c + t < a.N) orow[c + t] = f32_to_bf16(v[t]);
+                        }
+                    }
+            }
+        } else if constexpr (EPI == EPI_RESID) {
             // out[row][col] += acc: per 32-row block all 16 x TN loads are issued
             // before the adds and stores.
             float* out = reinterpret_cast<float*>(a.out);
