@@ -162,6 +162,50 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// Wave-wide reductions on DPP lane moves (no LDS traffic), the total read
+// from lane 63: within each quad, then 8 and 16 lanes (mirrors), then rows
+// 0+1 into row 1 and rows 2+3 into row 3 (broadcast of lane 15 of the row
+// below), then row 3 += lane 31.  A fixed order, so the result is the same on
+// every call with the same inputs.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ float dpp_f(float v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROWS, 0xF, false));
+#else
+    return v;
+#endif
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    v += dpp_f<0xB1>(v);            // quad_perm [1,0,3,2]
+    v += dpp_f<0x4E>(v);            // quad_perm [2,3,0,1]
+    v += dpp_f<0x141>(v);           // row_half_mirror
+    v += dpp_f<0x140>(v);           // row_mirror
+    v += dpp_f<0x142, 0xA>(v);      // row_bcast:15 into rows 1, 3
+    v += dpp_f<0x143, 0xC>(v);      // row_bcast:31 into rows 2, 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+#else
+    return v;
+#endif
+}
+__device__ __forceinline__ float wave_max_dpp(float v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    v = fmaxf(v, dpp_f<0xB1>(v));
+    v = fmaxf(v, dpp_f<0x4E>(v));
+    v = fmaxf(v, dpp_f<0x141>(v));
+    v = fmaxf(v, dpp_f<0x140>(v));
+    // rows outside the mask keep v (max with -inf from the zero-filled move
+    // would be wrong for all-negative inputs), hence the explicit select
+    const float b15 = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x142, 0xA, 0xF, false));
+    v = fmaxf(v, b15);
+    const float b31 = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x143, 0xC, 0xF, false));
+    v = fmaxf(v, b31);
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+#else
+    return v;
+#endif
+}
+
 // Online-softmax partial over a set of logits: running max m, the lowest index
 // attaining it, and s = sum exp(z - m).  merge() is associative up to float
 // rounding and keeps the lower index on equal maxima.

@@ -8,143 +8,172 @@
 
 namespace {
 
-// Router + top-k for 32 tokens per workgroup (16 waves).
+// XOR key of the 16-byte chunks of a 128-byte LDS row: 32 consecutive rows
+// read at one logical chunk hit distinct banks.
+__device__ __forceinline__ int rkey(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+// Router + top-k for 32 tokens per workgroup (8 waves).
 // z^T[e][t] = sum_c Wr[e][c] h[t][c] on v_mfma_f32_32x32x16_bf16 with experts
-// as rows (NB <= 16 blocks of 32) and tokens as columns; the reduction
-// dimension is split over 16 / NB waves per block and the parts are added in a
-// fixed order.  Each wave then selects for 2 tokens; lane r < k
-// records selection r with its rank among this workgroup's selections of the
-// same expert (LDS counter), and the workgroup's per-expert counts go to
-// wg_counts[E][workgroup].  Ranks only order rows inside an expert's group.
+// as rows (NB <= 8 blocks of 32) and tokens as columns.  K advances 64
+// columns at a time through 3 to 8 LDS stages that the waves fill with buffer
+// loads straight from global memory (whole 128-byte row segments, 16-byte
+// chunks XOR-swizzled), so every byte of h and Wr is fetched once per
+// workgroup in full cache lines.  Each expert block's 16-wide K steps are
+// dealt round-robin to 8 / NB waves and the parts are added in a fixed order.
+// Each wave then selects for 4 tokens; lane r < k records selection r with its
+// rank among this workgroup's selections of the same expert (LDS counter), and
+// the workgroup's per-expert counts go to wg_counts[E][workgroup].  Ranks only
+// order rows inside an expert's group.
 template <int NB>
-__global__ __launch_bounds__(1024) void router_topk_kernel(const bf16_t* __restrict__ h, const bf16_t* __restrict__ Wr,
-                                                          int T, int d, int E, int k, int32_t* __restrict__ ids,
-                                                          float* __restrict__ wts, int32_t* __restrict__ pos,
-                                                          int32_t* __restrict__ wg_counts) {
-    constexpr int NW = 16;                           // waves
+__global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restrict__ h, const bf16_t* __restrict__ Wr,
+                                                         int T, int d, int E, int k, int32_t* __restrict__ ids,
+                                                         float* __restrict__ wts, int32_t* __restrict__ pos,
+                                                         int32_t* __restrict__ wg_counts) {
+    constexpr int NW = 8;                            // waves
     static_assert(NB >= 1 && NB <= NW, "expert blocks");
     constexpr int KSPLIT = NW / NB;                  // waves sharing an expert block
-    constexpr int BPW = 1;                           // expert blocks per wave
     constexpr int EP = NB * 32;                      // padded expert count (LDS row)
     constexpr int ZROW = EP + 4;                     // row stride: 16-byte aligned, 4 banks of skew
-    __shared__ __attribute__((aligned(16))) float zs[KSPLIT][32][ZROW];
+    constexpr int ROWB = 128;                        // bytes per LDS row: 64 K columns
+    constexpr int H_BYTES = 32 * ROWB, STAGE = H_BYTES + EP * ROWB;
+    // Stages: as many as fit in 96 KB (3 to 8), so that several K chunks
+    // are in flight while one is multiplied.
+    constexpr int NS = 96 * 1024 / STAGE < 3 ? 3 : (96 * 1024 / STAGE > 8 ? 8 : 96 * 1024 / STAGE);
+    constexpr int NBLK = STAGE / 1024;               // 1 KB copy blocks per stage (8 rows each)
+    constexpr int NI = (NBLK + NW - 1) / NW;         // copies per wave and stage (the last block repeats)
+    constexpr int ZBYTES = KSPLIT * 32 * ZROW * 4 + 32 * EP * 8;
+    constexpr int LBYTES = NS * STAGE > ZBYTES ? NS * STAGE : ZBYTES;
+    __shared__ __attribute__((aligned(16))) char smem[LBYTES];   // K stages, then logit parts and keys
     __shared__ int lcnt[EP];
+    typedef float zrow_t[32][ZROW];
+    zrow_t* zs = reinterpret_cast<zrow_t*>(smem);
+    uint64_t* keys = reinterpret_cast<uint64_t*>(smem + KSPLIT * 32 * ZROW * 4);   // [32][EP]
 
-    // The wave index is made scalar so that branches on it (the K-batch tail
-    // below) are real branches: an MFMA under an EXEC mask still accumulates.
+    // The wave index is made scalar so that branches on it are real
+    // branches: an MFMA under an EXEC mask still accumulates.
     const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
     const int g = lane >> 5, j = lane & 31;
     const int t0 = blockIdx.x * 32;
-    const int blk0 = (wave / KSPLIT) * BPW, kc = wave % KSPLIT;
-    // K share of this wave: whole 16-wide steps, the last share may be short or empty.
-    const int kspan = (d / 16 + KSPLIT - 1) / KSPLIT * 16, kbeg = kc * kspan;
-    const int kend = min(kbeg + kspan, d);
-
+    const int blk0 = wave / KSPLIT, kc = wave % KSPLIT;
     for (int e = threadIdx.x; e < EP; e += NW * 64) lcnt[e] = 0;
-    const bf16_t* hrow = h + (int64_t)min(t0 + j, T - 1) * d + g * 8;
-    const bf16_t* wrow[BPW];
+
+    // Copy block q of a stage: q < 4 holds token rows 8q .. 8q+7 of h, the
+    // others expert rows of Wr (rows past T or E repeat the last one).
+    const buf_rsrc_t h_rsrc = make_rsrc(h), w_rsrc = make_rsrc(Wr);
+    uint32_t off[NI];
+    bool is_h[NI];
+    int dst[NI];
 #pragma unroll
-    for (int b = 0; b < BPW; ++b)                    // rows past E: clamped, their logits unused
-        wrow[b] = Wr + (int64_t)min((blk0 + b) * 32 + j, E - 1) * d + g * 8;
-    f32x16 acc[BPW];
-#pragma unroll
-    for (int b = 0; b < BPW; ++b)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
-    // K in batches of U steps; the fragments of batch n+1 are loaded while
-    // the MFMAs of batch n run (steps past the wave's span are clamped loads
-    // whose MFMAs are skipped).
-    constexpr int U = 4;
-    bf16x8 hb[2][U], wa[2][U][BPW];
-    auto load = [&](int buf, int c0) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = min(c0 + 16 * u, kend - 16);
-            hb[buf][u] = *reinterpret_cast<const bf16x8*>(hrow + c);
-#pragma unroll
-            for (int b = 0; b < BPW; ++b) wa[buf][u][b] = *reinterpret_cast<const bf16x8*>(wrow[b] + c);
-        }
-    };
-    auto compute = [&](int buf, int c0) {
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (c0 + 16 * u < kend) {
-#pragma unroll
-                for (int b = 0; b < BPW; ++b) acc[b] = mfma32x32x16(wa[buf][u][b], hb[buf][u], acc[b]);
-            }
-    };
-    if (kbeg < kend) load(0, kbeg);
-    for (int c0 = kbeg; c0 < kend; c0 += 32 * U) {
-        if (c0 + 16 * U < kend) load(1, c0 + 16 * U);
-        compute(0, c0);
-        if (c0 + 16 * U >= kend) break;
-        if (c0 + 32 * U < kend) load(0, c0 + 32 * U);
-        compute(1, c0 + 16 * U);
+    for (int p = 0; p < NI; ++p) {
+        const int q = min(wave * NI + p, NBLK - 1);
+        const int r8 = lane >> 3, pc = lane & 7;
+        is_h[p] = q < 4;
+        const int row = is_h[p] ? q * 8 + r8 : (q - 4) * 8 + r8;
+        const int64_t grow = is_h[p] ? min(t0 + row, T - 1) : min(row, E - 1);
+        off[p] = (uint32_t)(grow * d * 2) + (uint32_t)((pc ^ rkey(row)) * 16);
+        dst[p] = q * 1024;
     }
-    // acc[b][e]: expert (blk0+b)*32 + 8*(e/4) + 4*g + e%4, token j
+    const lds_ptr_t lds = (lds_ptr_t)smem;
+    typedef __attribute__((address_space(3))) char lds_char;
+    typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
+    auto issue = [&](int c, int stage) {             // K columns 64c .. 64c+63 into a stage
 #pragma unroll
-    for (int b = 0; b < BPW; ++b)
+        for (int p = 0; p < NI; ++p)
+            lds_dma16_buf(is_h[p] ? h_rsrc : w_rsrc, off[p], c * ROWB, (lds_ptr_t)((lds_char*)lds + stage * STAGE + dst[p]));
+    };
+
+    f32x16 acc;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) zs[kc][j][(blk0 + b) * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = acc[b][e];
+    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+    const int nk = d / 64;
+    const int hfrag = j * ROWB, wfrag = H_BYTES + (blk0 * 32 + j) * ROWB, key = rkey(j);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) issue(min(s, nk - 1), s);
+    for (int c = 0; c < nk; ++c) {
+        // own copies of K chunk c landed (later chunks may fly), then
+        // everyone's; the stage of chunk c-1 is free for chunk c+NS-1
+        if (c == 0) wait_vmcnt<NI * (NS - 1)>();
+        else wait_vmcnt<NI * (NS - 2)>();
+        __syncthreads();
+        if (c > 0) issue(min(c + NS - 1, nk - 1), (c + NS - 1) % NS);
+        const int sb = (c % NS) * STAGE;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            if ((c * 4 + ks) % KSPLIT != kc) continue;   // wave-uniform
+            const int co = ((2 * ks + g) ^ key) << 4;
+            const bf16x8 wf = *(lds_frag*)((lds_char*)lds + sb + wfrag + co);
+            const bf16x8 hf = *(lds_frag*)((lds_char*)lds + sb + hfrag + co);
+            acc = mfma32x32x16(wf, hf, acc);
+        }
+    }
+    wait_all_memory();                               // no copy may land in the logit parts
+    __syncthreads();
+    // acc[e]: expert blk0*32 + 8*(e/4) + 4*g + e%4, token j
+#pragma unroll
+    for (int e = 0; e < 16; ++e) zs[kc][j][blk0 * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = acc[e];
     __syncthreads();
     // Sum the K parts in a fixed order; logits of experts >= E become -inf,
-    // and so does a NaN logit, so that the rank order below stays total and
-    // every token receives exactly k distinct experts whatever its input.
+    // and so does a NaN logit, so that the order below stays total and every
+    // token receives exactly k distinct experts whatever its input.  Each
+    // (token, expert) also gets a 64-bit key: the logit's bits made orderable
+    // as an unsigned integer above the complement of the expert id, so that
+    // "larger logit, or equal logit and lower id" is one unsigned compare.
     for (int i = threadIdx.x; i < 32 * EP; i += NW * 64) {
         const int tt = i / EP, e = i - tt * EP;
         float z = zs[0][tt][e];
 #pragma unroll
         for (int s = 1; s < KSPLIT; ++s) z += zs[s][tt][e];
-        zs[0][tt][e] = (e < E && z == z) ? z : -INFINITY;
+        z = (e < E && z == z) ? z + 0.f : -INFINITY;         // (+0.f: -0 and +0 compare equal)
+        zs[0][tt][e] = z;
+        const uint32_t u = __float_as_uint(z);
+        const uint32_t ord = u ^ ((u >> 31) ? 0xffffffffu : 0x80000000u);
+        keys[tt * EP + e] = ((uint64_t)ord << 32) | (uint32_t)~e;
     }
     __syncthreads();
 
     // Top-k per token, one wave per token at a time; lane owns experts
     // lane + 64q.  p = softmax(z) over the E experts; expert e is selection
-    // r = #{e' : z[e'] > z[e] or (z[e'] == z[e] and e' < e)} if r < k (the k
-    // largest logits, ties -> lower id, in descending order); the selected
-    // probabilities are renormalised to sum to one.
+    // r = #{e' : key[e'] > key[e]} if r < k (the k largest logits, ties ->
+    // lower id, in descending order); the selected probabilities are
+    // renormalised to sum to one.
     constexpr int NQ = (EP + 63) / 64;
     constexpr int TPW = 32 / NW;                     // tokens per wave
     for (int i = 0; i < TPW; ++i) {
         const int tt = wave * TPW + i, t = t0 + tt;
         const float* z = zs[0][tt];
+        const uint64_t* kr = keys + tt * EP;
         float v[NQ];
+        uint64_t kq[NQ];
         int rank[NQ];
+        float vm = -INFINITY;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            v[q] = (lane + 64 * q < E) ? z[lane + 64 * q] : -INFINITY;
+            const int e = lane + 64 * q;
+            v[q] = e < E ? z[e] : -INFINITY;
+            kq[q] = e < EP ? kr[e] : 0;
             rank[q] = 0;
+            vm = fmaxf(vm, v[q]);
         }
-        // z is -inf past E up to a multiple of 4: reads are wave-uniform LDS
-        // broadcasts, four logits at a time.
-        const int E4 = (E + 3) & ~3;
-        float m = -INFINITY;
+        // keys are wave-uniform LDS broadcasts, two per 16-byte read
 #pragma unroll 4
-        for (int e2 = 0; e2 < E4; e2 += 4) {
-            const float4 z4 = *reinterpret_cast<const float4*>(z + e2);
-            const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
-            m = fmaxf(fmaxf(m, fmaxf(zz[0], zz[1])), fmaxf(zz[2], zz[3]));
+        for (int e2 = 0; e2 < EP; e2 += 2) {
+            const uint64_t k0 = kr[e2], k1 = kr[e2 + 1];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) {
-                    const int e = lane + 64 * q;
-                    rank[q] += (zz[u] > v[q] || (zz[u] == v[q] && e2 + u < e)) ? 1 : 0;
-                }
+            for (int q = 0; q < NQ; ++q) rank[q] += (k0 > kq[q]) + (k1 > kq[q]);
         }
+        const float m = wave_max_dpp(vm);
         float p[NQ], own = 0.f;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             p[q] = (lane + 64 * q < E) ? __expf(v[q] - m) : 0.f;
             own += p[q];
         }
-        const float sum = wave_sum(own);
+        const float sum = wave_sum_dpp(own);
         float psel = 0.f;
 #pragma unroll
         for (int q = 0; q < NQ; ++q)
             if (rank[q] < k) psel += p[q] / sum;
-        const float psum = wave_sum(psel);
+        const float psum = wave_sum_dpp(psel);
         if (t < T) {
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
@@ -306,7 +335,7 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
 hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, int E, int k, int32_t* ids,
                               float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st) {
     if (E < 1 || E > 256 || k < 1 || k > 8 || k > E || d % 64 != 0 || T < 1) return hipErrorInvalidValue;
-    const dim3 grid((T + 31) / 32), block(1024);
+    const dim3 grid((T + 31) / 32), block(512);
     if (E <= 32)
         hipLaunchKernelGGL(router_topk_kernel<1>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
     else if (E <= 64)
