@@ -162,6 +162,44 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// 1 / sqrt(mean(x^2) + eps) of a row held by a workgroup of up to 4 waves,
+// from each thread's partial sum of squares: per-wave sums, then the waves in
+// order (a fixed order: every kernel that normalises a row this way gets the
+// same bits for the same row).
+__device__ __forceinline__ float block_rms_scale(float ss, int d, float eps) {
+    __shared__ float red[4];
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    float tot = 0.f;
+    const int nw = blockDim.x >> 6;
+    for (int w = 0; w < nw; ++w) tot += red[w];
+    return 1.f / sqrtf(tot / (float)d + eps);
+}
+
+// hr = bf16(xr * r * g) for the chunks of 8 this thread owns in a row
+// normalised by a workgroup (chunk i*8 .. i*8+7 for i = thread + k * threads).
+__device__ __forceinline__ void rms_store_row(const float* xr, const bf16_t* __restrict__ g, bf16_t* __restrict__ hr,
+                                              int d, float r) {
+    for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(xr + i);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(xr + i + 4);
+        const u32x4 gg = *reinterpret_cast<const u32x4*>(g + i);
+        float gv[8];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            gv[2 * w] = __uint_as_float(gg[w] << 16);
+            gv[2 * w + 1] = __uint_as_float(gg[w] & 0xffff0000u);
+        }
+        u32x4 o;
+        o[0] = pack_bf16x2(a[0] * r * gv[0], a[1] * r * gv[1]);
+        o[1] = pack_bf16x2(a[2] * r * gv[2], a[3] * r * gv[3]);
+        o[2] = pack_bf16x2(b[0] * r * gv[4], b[1] * r * gv[5]);
+        o[3] = pack_bf16x2(b[2] * r * gv[6], b[3] * r * gv[7]);
+        *reinterpret_cast<u32x4*>(hr + i) = o;
+    }
+}
+
 // Wave-wide reductions on DPP lane moves (no LDS traffic), the total read
 // from lane 63: within each quad, then 8 and 16 lanes (mirrors), then rows
 // 0+1 into row 1 and rows 2+3 into row 3 (broadcast of lane 15 of the row

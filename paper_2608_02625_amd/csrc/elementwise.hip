@@ -31,7 +31,6 @@ __global__ void embed_kernel(const int32_t* __restrict__ tok, const bf16_t* __re
 // h = bf16(x / sqrt(mean(x^2) + eps) * g), fp32 math; one workgroup (256) per row.
 __device__ __forceinline__ void rmsnorm_row(const float* __restrict__ xr, const bf16_t* __restrict__ g,
                                             bf16_t* __restrict__ hr, int d, float eps) {
-    __shared__ float red[4];
     float ss = 0.f;
     for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
         const f32x4 a = *reinterpret_cast<const f32x4*>(xr + i);
@@ -39,30 +38,7 @@ __device__ __forceinline__ void rmsnorm_row(const float* __restrict__ xr, const 
         ss += a[0] * a[0] + a[1] * a[1] + a[2] * a[2] + a[3] * a[3];
         ss += b[0] * b[0] + b[1] * b[1] + b[2] * b[2] + b[3] * b[3];
     }
-    ss = wave_sum(ss);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-    __syncthreads();
-    float tot = 0.f;
-    const int nw = blockDim.x >> 6;
-    for (int w = 0; w < nw; ++w) tot += red[w];
-    const float r = 1.f / sqrtf(tot / (float)d + eps);
-    for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
-        const f32x4 a = *reinterpret_cast<const f32x4*>(xr + i);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(xr + i + 4);
-        const u32x4 gg = *reinterpret_cast<const u32x4*>(g + i);
-        float gv[8];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            gv[2 * w] = __uint_as_float(gg[w] << 16);
-            gv[2 * w + 1] = __uint_as_float(gg[w] & 0xffff0000u);
-        }
-        u32x4 o;
-        o[0] = pack_bf16x2(a[0] * r * gv[0], a[1] * r * gv[1]);
-        o[1] = pack_bf16x2(a[2] * r * gv[2], a[3] * r * gv[3]);
-        o[2] = pack_bf16x2(b[0] * r * gv[4], b[1] * r * gv[5]);
-        o[3] = pack_bf16x2(b[2] * r * gv[6], b[3] * r * gv[7]);
-        *reinterpret_cast<u32x4*>(hr + i) = o;
-    }
+    rms_store_row(xr, g, hr, d, block_rms_scale(ss, d, eps));
 }
 
 __global__ void rmsnorm_kernel(const float* __restrict__ x, const bf16_t* __restrict__ g,

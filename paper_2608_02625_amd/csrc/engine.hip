@@ -251,6 +251,7 @@ struct Ctx {
     Workspace w;
     hipStream_t st;
     int B, P, D, S, T, R;
+    bool h_ready = false;           // h already holds the next block's normalised input
     template <class Tp>
     Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
     const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
@@ -328,7 +329,8 @@ dlm_status run_layer(Ctx& x, int l) {
     bf16_t* v = x.at<bf16_t>(x.w.v);
     bf16_t* attn = x.at<bf16_t>(x.w.attn);
 
-    LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g1), h, x.T, d, c.norm_eps, x.st));
+    if (!x.h_ready) LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g1), h, x.T, d, c.norm_eps, x.st));
+    x.h_ready = false;
     {
         // Transposed: rows = the (H + 2 KV) * hd output features, columns = tokens.
         const int N = (H + 2 * KV) * hd;
@@ -420,7 +422,11 @@ dlm_status run_layer(Ctx& x, int l) {
         a.variant = 11;
         TRY(gemm(x, "gemm_expert_down", a, EPI_BF16, true, kExpertBM, kExpertBN, x.w.max_tiles));
     }
-    LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d, x.st));
+    // The combine also normalises each finished row for the next block.
+    const bool fuse = l + 1 < c.n_layers;
+    LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d,
+                                        fuse ? x.wt(x.m->plan.layers[l + 1].g1) : nullptr, h, c.norm_eps, x.st));
+    x.h_ready = fuse;
     return DLM_OK;
 }
 

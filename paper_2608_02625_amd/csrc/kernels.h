@@ -107,6 +107,8 @@ hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared
                            int32_t* grp_off, int2* tile_tab, int32_t* n_tiles, int32_t* slot, int32_t* a_rows,
                            hipStream_t st);
 // x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[shared rows]
+// With g_next != nullptr, also writes h_next = RMSNorm(x) * g_next (bf16) for
+// the next block (the combine holds each finished residual row).
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
                     const int32_t* grp_off, int T, int k, int E, int n_shared, int d,
-                    hipStream_t st);
+                    const bf16_t* g_next, bf16_t* h_next, float eps, hipStream_t st);

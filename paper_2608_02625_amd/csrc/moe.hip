@@ -290,10 +290,12 @@ __global__ __launch_bounds__(256) void dispatch_scatter_kernel(const int32_t* __
 }
 
 // x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[grp_off[E+s] + t], fixed order.
+// With g_next, also the next block's input norm h[t] = bf16(x[t] / rms * g_next)
+// (the same arithmetic, in the same order, as the stand-alone RMSNorm).
 __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__ Y,
                                const int32_t* __restrict__ slot, const float* __restrict__ w,
                                const int32_t* __restrict__ grp_off, int k, int E, int n_shared,
-                               int d) {
+                               int d, const bf16_t* __restrict__ g_next, bf16_t* __restrict__ h_next, float eps) {
     const int t = blockIdx.x;
     int rows[9];
     float wt[9];
@@ -307,6 +309,7 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
         wt[nrow++] = 1.f;
     }
     float* xr = x + (int64_t)t * d;
+    float ss = 0.f;
     for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
         for (int r = 0; r < nrow; ++r) {
@@ -327,7 +330,10 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
         }
         *reinterpret_cast<f32x4*>(xr + i) = a;
         *reinterpret_cast<f32x4*>(xr + i + 4) = b;
+        ss += a[0] * a[0] + a[1] * a[1] + a[2] * a[2] + a[3] * a[3];
+        ss += b[0] * b[0] + b[1] * b[1] + b[2] * b[2] + b[3] * b[3];
     }
+    if (g_next) rms_store_row(xr, g_next, h_next + (int64_t)t * d, d, block_rms_scale(ss, d, eps));
 }
 
 }  // namespace
@@ -361,7 +367,8 @@ hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared
 }
 
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
-                    const int32_t* grp_off, int T, int k, int E, int n_shared, int d, hipStream_t st) {
+                    const int32_t* grp_off, int T, int k, int E, int n_shared, int d, const bf16_t* g_next,
+                    bf16_t* h_next, float eps, hipStream_t st) {
     hipLaunchKernelGGL(combine_kernel, dim3(T), dim3(256), 0, st, x, Y, slot, w, grp_off, k, E,
-                       n_shared, d);
+                       n_shared, d, g_next, h_next, eps);
 }
