@@ -144,6 +144,44 @@ dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t d
                       void* hip_stream, dlm_stats* h_stats);
 
 /*
+ * Editing rule with separate thresholds and an EOS stop (App. C.4: the native
+ * token-editing rule ends a refinement early once no confident edit remains or
+ * an EOS token is produced; the reading used here):
+ *   a [MASK] draft slot takes t* when t* != mask_id and conf >= unmask_threshold;
+ *   a real-token draft slot takes t* when t* != mask_id and conf >= edit_threshold;
+ *   with eos_id >= 0, a pass that writes eos_id into at least one draft slot
+ *   (a slot that did not already hold it) ends dlm_refine_ex after that pass.
+ * unmask_threshold == edit_threshold with eos_id < 0 is the rule of
+ * dlm_refine_step.  Thresholds must not be NaN; eos_id < vocab.
+ */
+typedef struct dlm_edit_rule {
+    float unmask_threshold;
+    float edit_threshold;
+    int32_t eos_id;            /* < 0: no EOS stop */
+} dlm_edit_rule;
+
+/*
+ * dlm_refine_step under *rule (host pointer).  d_eos_written (device int32,
+ * may be NULL) receives the number of draft slots this pass set to eos_id
+ * (0 when rule->eos_id < 0).  Other arguments as dlm_refine_step.
+ */
+dlm_status dlm_refine_step_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                              int32_t* d_tokens, const dlm_edit_rule* rule, void* d_workspace,
+                              size_t workspace_bytes, void* hip_stream, int32_t* d_top1, float* d_conf,
+                              dlm_stats* d_stats, int32_t* d_eos_written);
+
+/*
+ * dlm_refine under *rule: stops after a pass that changed no slot, or (eos_id
+ * >= 0) after a pass that wrote eos_id into a draft slot.  h_stop_reason (host,
+ * may be NULL): 0 = pass budget used up (or n_steps = 0), 1 = a pass changed
+ * nothing, 2 = EOS written.  Other arguments as dlm_refine.
+ */
+dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                         const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
+                         const dlm_edit_rule* rule, void* d_workspace, size_t workspace_bytes,
+                         void* hip_stream, dlm_stats* h_stats, int32_t* h_stop_reason);
+
+/*
  * Test hooks (same kernels as dlm_refine_step, intermediate results exposed).
  *
  * dlm_debug_forward: forward over d_tokens without the reduction; writes the

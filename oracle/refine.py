@@ -287,21 +287,85 @@ def edit_rule(draft: np.ndarray, top1: np.ndarray, conf: np.ndarray, tau: float,
     return new, n_unmasked, n_edited
 
 
-def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float, decide_bf16: bool = True):
-    """One refinement pass over tokens [B, S] (prompt in [0, P), draft in [P, S))."""
-    shape = W.shape
+def _reduce_draft(W, tokens: np.ndarray, prompt_len: int, decide_bf16: bool):
+    """Forward over the whole sequence, then top-1 and confidence of every draft position."""
     B, S = tokens.shape
     D = S - prompt_len
     x = forward(W, tokens, decide_bf16=decide_bf16)
     red = lm_head_reduce(W, x[:, prompt_len:, :].reshape(B * D, -1), decide_bf16=decide_bf16)
-    top1 = red["top1"].reshape(B, D)
-    conf = red["conf"].reshape(B, D)
-    new_draft, n_unm, n_edit = edit_rule(tokens[:, prompt_len:], top1, conf, tau, shape.mask_id)
+    return {"top1": red["top1"].reshape(B, D), "conf": red["conf"].reshape(B, D),
+            "max_logit": red["max_logit"].reshape(B, D), "margin": red["margin"].reshape(B, D)}
+
+
+def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float, decide_bf16: bool = True):
+    """One refinement pass over tokens [B, S] (prompt in [0, P), draft in [P, S))."""
+    info = _reduce_draft(W, tokens, prompt_len, decide_bf16)
+    new_draft, n_unm, n_edit = edit_rule(tokens[:, prompt_len:], info["top1"], info["conf"], tau, W.shape.mask_id)
     out = tokens.copy()
     out[:, prompt_len:] = new_draft
-    info = {"top1": top1, "conf": conf, "max_logit": red["max_logit"].reshape(B, D),
-            "margin": red["margin"].reshape(B, D), "n_unmasked": n_unm, "n_edited": n_edit}
+    info.update({"n_unmasked": n_unm, "n_edited": n_edit})
     return out, info
+
+
+# ------------------------------------------- two thresholds and the EOS stop
+
+def edit_rule_ex(draft: np.ndarray, top1: np.ndarray, conf: np.ndarray, tau_unmask: float, tau_edit: float,
+                 mask_id: int, eos_id: int = -1):
+    """Editing rule with separate thresholds (App. C.4 names the native
+    token-editing rule and its early end: no confident edit left, or an EOS
+    token produced; the reading used here): from one forward, a [MASK] slot
+    takes its top-1 when top1 != mask_id and conf >= tau_unmask, a real-token
+    slot when top1 != mask_id and conf >= tau_edit.  Also returns how many
+    slots were newly set to eos_id (0 when eos_id < 0)."""
+    is_mask = draft == mask_id
+    thr = np.where(is_mask, tau_unmask, tau_edit)
+    take = (top1 != mask_id) & (conf >= thr)
+    new = np.where(take, top1, draft).astype(draft.dtype)
+    changed = new != draft
+    n_unmasked = int(np.sum(changed & is_mask))
+    n_edited = int(np.sum(changed & ~is_mask))
+    n_eos = int(np.sum(changed & (new == eos_id))) if eos_id >= 0 else 0
+    return new, n_unmasked, n_edited, n_eos
+
+
+def refine_step_ex(W, tokens: np.ndarray, prompt_len: int, tau_unmask: float, tau_edit: float, eos_id: int = -1,
+                   decide_bf16: bool = True):
+    """One refinement pass under edit_rule_ex."""
+    info = _reduce_draft(W, tokens, prompt_len, decide_bf16)
+    new_draft, n_unm, n_edit, n_eos = edit_rule_ex(tokens[:, prompt_len:], info["top1"], info["conf"],
+                                                   tau_unmask, tau_edit, W.shape.mask_id, eos_id)
+    out = tokens.copy()
+    out[:, prompt_len:] = new_draft
+    info.update({"n_unmasked": n_unm, "n_edited": n_edit, "n_eos": n_eos})
+    return out, info
+
+
+def refine_ex(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_steps: int,
+              tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = True):
+    """refine() under edit_rule_ex: stops after a pass that changed nothing
+    (stop_reason 1) or, with eos_id >= 0, after a pass that wrote eos_id into a
+    draft slot (stop_reason 2); 0 when the pass budget ran out."""
+    shape = W.shape
+    P = prompt.shape[1]
+    d = draft.copy()
+    if mask is not None:
+        d[mask] = shape.mask_id
+    tokens = np.concatenate([prompt, d], axis=1).astype(np.int32)
+    stats = {"steps_run": 0, "n_unmasked": 0, "n_edited": 0, "stop_reason": 0, "per_step": []}
+    for _ in range(n_steps):
+        tokens, info = refine_step_ex(W, tokens, P, tau_unmask, tau_edit, eos_id, decide_bf16)
+        stats["steps_run"] += 1
+        stats["n_unmasked"] += info["n_unmasked"]
+        stats["n_edited"] += info["n_edited"]
+        stats["per_step"].append(info)
+        if info["n_unmasked"] + info["n_edited"] == 0:
+            stats["stop_reason"] = 1
+            break
+        if eos_id >= 0 and info["n_eos"] > 0:
+            stats["stop_reason"] = 2
+            break
+    stats["n_masked_left"] = int(np.sum(tokens[:, P:] == shape.mask_id))
+    return tokens[:, P:].copy(), stats
 
 
 def refine(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_steps: int,

@@ -38,6 +38,11 @@ class DlmStats(ctypes.Structure):
 
 
 # (name, restype, argtypes) of every entry point in include/dlm.h
+class DlmEditRule(ctypes.Structure):
+    _fields_ = [("unmask_threshold", ctypes.c_float), ("edit_threshold", ctypes.c_float),
+                ("eos_id", ctypes.c_int32)]
+
+
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
 _F = ctypes.c_float
@@ -49,6 +54,9 @@ SIGNATURES = [
     ("dlm_load_synthetic_weights", _I, [_CFG, ctypes.c_uint64, _P, _SZ, _P, ctypes.POINTER(_P)]),
     ("dlm_refine_step", _I, [_P, _I, _I, _I, _P, _F, _P, _SZ, _P, _P, _P, _P]),
     ("dlm_refine", _I, [_P, _I, _I, _I, _P, _P, _P, _I, _F, _P, _SZ, _P, ctypes.POINTER(DlmStats)]),
+    ("dlm_refine_step_ex", _I, [_P, _I, _I, _I, _P, ctypes.POINTER(DlmEditRule), _P, _SZ, _P, _P, _P, _P, _P]),
+    ("dlm_refine_ex", _I, [_P, _I, _I, _I, _P, _P, _P, _I, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
+                           ctypes.POINTER(DlmStats), ctypes.POINTER(_I)]),
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
     ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),

@@ -90,27 +90,31 @@ __global__ __launch_bounds__(256) void lmhead_merge_kernel(const float4* __restr
 // Threshold rule, all draft slots at once from the same forward pass.
 __global__ void edit_kernel(int32_t* __restrict__ tokens, int S, int P, int D,
                             const int32_t* __restrict__ top1, const float* __restrict__ conf,
-                            float threshold, int mask_id, int32_t* __restrict__ counters,
+                            float thr_unmask, float thr_edit, int mask_id, int eos_id,
+                            int32_t* __restrict__ counters, int32_t* __restrict__ eos_count,
                             int32_t* __restrict__ out_top1, float* __restrict__ out_conf, int n) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    int unm = 0, edt = 0;
+    int unm = 0, edt = 0, eos = 0;
     if (r < n) {
         const int b = r / D, i = r - b * D;
         int32_t* slot = tokens + (int64_t)b * S + P + i;
         const int32_t cur = *slot;
         const int32_t t = top1[r];
         const float c = conf[r];
-        if (t != mask_id && c >= threshold && t != cur) {
+        const float thr = cur == mask_id ? thr_unmask : thr_edit;
+        if (t != mask_id && c >= thr && t != cur) {
             *slot = t;
             if (cur == mask_id) unm = 1; else edt = 1;
+            eos = t == eos_id;
         }
         if (out_top1) out_top1[r] = t;
         if (out_conf) out_conf[r] = c;
     }
-    const unsigned long long bu = __ballot(unm), be = __ballot(edt);
+    const unsigned long long bu = __ballot(unm), be = __ballot(edt), bx = __ballot(eos);
     if ((threadIdx.x & 63) == 0) {
         if (bu) atomicAdd(&counters[0], (int)__popcll(bu));
         if (be) atomicAdd(&counters[1], (int)__popcll(be));
+        if (bx && eos_count) atomicAdd(eos_count, (int)__popcll(bx));
     }
 }
 
@@ -188,11 +192,11 @@ void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* to
 }
 
 void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top1, const float* conf,
-                 float threshold, int mask_id, int32_t* counters, int32_t* out_top1,
-                 float* out_conf, hipStream_t st) {
+                 float thr_unmask, float thr_edit, int mask_id, int eos_id, int32_t* counters, int32_t* eos_count,
+                 int32_t* out_top1, float* out_conf, hipStream_t st) {
     const int n = B * D;
     hipLaunchKernelGGL(edit_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, S, P, D, top1,
-                       conf, threshold, mask_id, counters, out_top1, out_conf, n);
+                       conf, thr_unmask, thr_edit, mask_id, eos_id, counters, eos_count, out_top1, out_conf, n);
 }
 
 void launch_apply_mask(const int32_t* prompt, const int32_t* draft, const uint8_t* mask,

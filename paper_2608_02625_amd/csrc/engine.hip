@@ -208,7 +208,7 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
     w.top1 = add(R * 4);
     w.conf = add(R * 4);
     w.maxlogit = add(R * 4);
-    w.counters = add(sizeof(dlm_stats));
+    w.counters = add(sizeof(dlm_stats) + 16);          // pass counters, then the EOS count
     w.tokens = add(T * 4);
     return w;
 }
@@ -477,17 +477,27 @@ Ctx ctx_for(dlm_model* m, int B, int P, int D, void* ws, const Workspace& w, voi
     return x;
 }
 
-dlm_status step_impl(Ctx& x, int32_t* tokens, float threshold, int32_t* top1_out, float* conf_out,
-                     dlm_stats* stats_out) {
+dlm_status step_impl(Ctx& x, int32_t* tokens, const dlm_edit_rule& rule, int32_t* top1_out, float* conf_out,
+                     dlm_stats* stats_out, int32_t* eos_out = nullptr) {
     const dlm_config& c = x.c;
     int32_t* counters = x.at<int32_t>(x.w.counters);
-    LAUNCH(x, "zero", launch_zero_i32(counters, 4, x.st));
+    int32_t* eos = counters + 4;
+    LAUNCH(x, "zero", launch_zero_i32(counters, 5, x.st));
     TRY(run_prologue(x, tokens));
     for (int l = 0; l < c.n_layers; ++l) TRY(run_layer(x, l));
     TRY(run_head(x, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf), x.at<float>(x.w.maxlogit), nullptr));
     LAUNCH(x, "edit", launch_edit(tokens, x.B, x.S, x.P, x.D, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf),
-                                  threshold, c.mask_id, counters, top1_out, conf_out, x.st));
+                                  rule.unmask_threshold, rule.edit_threshold, c.mask_id, rule.eos_id, counters,
+                                  rule.eos_id >= 0 ? eos : nullptr, top1_out, conf_out, x.st));
     if (stats_out) HIP_TRY(hipMemcpyAsync(stats_out, counters, sizeof(dlm_stats), hipMemcpyDeviceToDevice, x.st));
+    if (eos_out) HIP_TRY(hipMemcpyAsync(eos_out, eos, 4, hipMemcpyDeviceToDevice, x.st));
+    return DLM_OK;
+}
+
+dlm_status check_rule(const dlm_config& c, const dlm_edit_rule* rule) {
+    if (!rule) return fail(DLM_ERR_INVALID_ARG, "rule is NULL");
+    if (isnan(rule->unmask_threshold) || isnan(rule->edit_threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    if (rule->eos_id >= c.vocab) return fail(DLM_ERR_INVALID_ARG, "eos_id >= vocab");
     return DLM_OK;
 }
 
@@ -540,41 +550,58 @@ dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void
     return DLM_OK;
 }
 
-dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
-                           int32_t* d_tokens, float threshold, void* d_workspace, size_t workspace_bytes,
-                           void* hip_stream, int32_t* d_top1, float* d_conf, dlm_stats* d_stats) {
+dlm_status dlm_refine_step_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                              int32_t* d_tokens, const dlm_edit_rule* rule, void* d_workspace,
+                              size_t workspace_bytes, void* hip_stream, int32_t* d_top1, float* d_conf,
+                              dlm_stats* d_stats, int32_t* d_eos_written) {
     Workspace w;
     TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
     if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
-    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    TRY(check_rule(m->cfg, rule));
     Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
-    return step_impl(x, d_tokens, threshold, d_top1, d_conf, d_stats);
+    return step_impl(x, d_tokens, *rule, d_top1, d_conf, d_stats, d_eos_written);
 }
 
-dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
-                      const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
-                      float threshold, void* d_workspace, size_t workspace_bytes, void* hip_stream,
-                      dlm_stats* h_stats) {
+dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                           int32_t* d_tokens, float threshold, void* d_workspace, size_t workspace_bytes,
+                           void* hip_stream, int32_t* d_top1, float* d_conf, dlm_stats* d_stats) {
+    const dlm_edit_rule rule{threshold, threshold, -1};
+    return dlm_refine_step_ex(m, batch, prompt_len, draft_len, d_tokens, &rule, d_workspace, workspace_bytes,
+                              hip_stream, d_top1, d_conf, d_stats, nullptr);
+}
+
+dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                         const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
+                         const dlm_edit_rule* rule, void* d_workspace, size_t workspace_bytes,
+                         void* hip_stream, dlm_stats* h_stats, int32_t* h_stop_reason) {
     Workspace w;
     TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
     if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
     if (n_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_steps < 0");
-    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    TRY(check_rule(m->cfg, rule));
     Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
     int32_t* tokens = x.at<int32_t>(w.tokens);
     int32_t* counters = x.at<int32_t>(w.counters);
     launch_apply_mask(d_prompt, d_draft, d_mask, tokens, batch, prompt_len, draft_len, m->cfg.mask_id, x.st);
     HIP_TRY(hipGetLastError());
     dlm_stats tot{0, 0, 0, 0};
+    int32_t reason = 0;
     for (int s = 0; s < n_steps; ++s) {
-        TRY(step_impl(x, tokens, threshold, nullptr, nullptr, nullptr));
-        dlm_stats st{};
-        HIP_TRY(hipMemcpyAsync(&st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
+        TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
+        int32_t st[5] = {};                           // the pass counters and the EOS count
+        HIP_TRY(hipMemcpyAsync(st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
         HIP_TRY(hipStreamSynchronize(x.st));
-        tot.n_unmasked += st.n_unmasked;
-        tot.n_edited += st.n_edited;
+        tot.n_unmasked += st[0];
+        tot.n_edited += st[1];
         tot.steps_run += 1;
-        if (st.n_unmasked + st.n_edited == 0) break;
+        if (st[0] + st[1] == 0) {
+            reason = 1;
+            break;
+        }
+        if (rule->eos_id >= 0 && st[4] > 0) {
+            reason = 2;
+            break;
+        }
     }
     launch_copy_draft_out(tokens, d_draft, batch, x.S, prompt_len, draft_len, x.st);
     launch_zero_i32(counters, 4, x.st);
@@ -585,7 +612,17 @@ dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t d
     HIP_TRY(hipStreamSynchronize(x.st));
     tot.n_masked_left = st.n_masked_left;
     if (h_stats) *h_stats = tot;
+    if (h_stop_reason) *h_stop_reason = reason;
     return DLM_OK;
+}
+
+dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                      const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
+                      float threshold, void* d_workspace, size_t workspace_bytes, void* hip_stream,
+                      dlm_stats* h_stats) {
+    const dlm_edit_rule rule{threshold, threshold, -1};
+    return dlm_refine_ex(m, batch, prompt_len, draft_len, d_prompt, d_draft, d_mask, n_steps, &rule, d_workspace,
+                         workspace_bytes, hip_stream, h_stats, nullptr);
 }
 
 dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,

@@ -79,9 +79,12 @@ void launch_rmsnorm_draft_rows(const float* x, const bf16_t* g, bf16_t* h, int B
                                int D, int d, float eps, hipStream_t st);
 void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* top1, float* conf,
                          float* max_logit, hipStream_t st);
+// Threshold update of every draft slot ([MASK] slots against thr_unmask,
+// real tokens against thr_edit); counters[0] += unmasked, counters[1] +=
+// edited, *eos_count (if not null) += slots newly set to eos_id.
 void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top1, const float* conf,
-                 float threshold, int mask_id, int32_t* counters, int32_t* out_top1,
-                 float* out_conf, hipStream_t st);
+                 float thr_unmask, float thr_edit, int mask_id, int eos_id, int32_t* counters,
+                 int32_t* eos_count, int32_t* out_top1, float* out_conf, hipStream_t st);
 void launch_apply_mask(const int32_t* prompt, const int32_t* draft, const uint8_t* mask,
                        int32_t* tokens, int B, int P, int D, int mask_id, hipStream_t st);
 void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, int P, int D,

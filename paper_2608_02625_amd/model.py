@@ -108,6 +108,40 @@ class Refiner:
                                   ctypes.byref(st)), "dlm_refine")
         return draft, st.as_dict()
 
+    def refine_step_ex(self, tokens: torch.Tensor, prompt_len: int, unmask_threshold: float,
+                       edit_threshold: float, eos_id: int = -1, top1: torch.Tensor | None = None,
+                       conf: torch.Tensor | None = None, stats: torch.Tensor | None = None,
+                       eos_written: torch.Tensor | None = None):
+        """One pass under the two-threshold rule (tokens int32 [B, S], updated in place)."""
+        B, S = tokens.shape
+        D = S - prompt_len
+        ws = self.workspace(B, prompt_len, D)
+        rule = _lib.DlmEditRule(float(unmask_threshold), float(edit_threshold), int(eos_id))
+        check(self.lib.dlm_refine_step_ex(self._handle, B, prompt_len, D, tokens.data_ptr(), ctypes.byref(rule),
+                                          ws.data_ptr(), ws.numel(), self.stream, _ptr(top1), _ptr(conf),
+                                          _ptr(stats), _ptr(eos_written)), "dlm_refine_step_ex")
+        return tokens
+
+    def refine_ex(self, prompt: torch.Tensor, draft: torch.Tensor, mask: torch.Tensor | None, n_steps: int,
+                  unmask_threshold: float, edit_threshold: float, eos_id: int = -1):
+        """refine() under the two-threshold rule with the EOS stop; the stats
+        gain stop_reason (0 budget, 1 no change, 2 EOS written)."""
+        B, P = prompt.shape
+        D = draft.shape[1]
+        ws = self.workspace(B, P, D)
+        m = None
+        if mask is not None:
+            m = mask.to(torch.uint8).contiguous()
+        st = DlmStats()
+        reason = ctypes.c_int32(-1)
+        rule = _lib.DlmEditRule(float(unmask_threshold), float(edit_threshold), int(eos_id))
+        check(self.lib.dlm_refine_ex(self._handle, B, P, D, prompt.data_ptr() if P else None, draft.data_ptr(),
+                                     _ptr(m), int(n_steps), ctypes.byref(rule), ws.data_ptr(), ws.numel(),
+                                     self.stream, ctypes.byref(st), ctypes.byref(reason)), "dlm_refine_ex")
+        out = st.as_dict()
+        out["stop_reason"] = int(reason.value)
+        return draft, out
+
     # -------------------------------------------------------------- test hooks
     def debug_forward(self, tokens: torch.Tensor, prompt_len: int, want_logits: bool = False):
         B, S = tokens.shape

@@ -184,6 +184,67 @@ def test_refine_tiny_sharp_trajectory(tiny_sharp):
     assert gst["n_masked_left"] == int(np.sum(got[:, P:] == s.mask_id))
 
 
+def test_refine_ex_two_thresholds_and_eos(tiny_sharp):
+    """Two-threshold rule (unmask at the 60th, edit at the 90th confidence
+    percentile) along the GPU's own trajectory: every pass agrees with the
+    oracle's pass on the same input at non-exempt positions (exemption by the
+    position's own threshold).  The loop entry point reproduces the trajectory;
+    with an EOS id that the first pass writes it ends after that pass."""
+    import oracle
+    torch = _torch()
+    w, s, R, W = tiny_sharp
+    prompt, draft, mask = make_inputs(w)
+    P, D = w.prompt_len, w.draft_len
+    margin = MARGIN * s.lm_head_scale
+    _, info0 = oracle.refine_step(W, _tokens(w, s), P, 1.0)
+    tu, te = (float(np.round(np.quantile(info0["conf"], q), 2)) for q in (0.6, 0.9))
+    log(f"[tiny sharp ex] unmask threshold {tu} edit threshold {te}")
+    g = _cuda_i32(_tokens(w, s))
+    traj, steps, first_written = [], 0, None
+    for step in range(w.n_steps):
+        cur = _np(g).copy()
+        ref_next, info = oracle.refine_step_ex(W, cur, P, tu, te)
+        eosw = torch.zeros(1, dtype=torch.int32, device="cuda")
+        stats = torch.zeros(4, dtype=torch.int32, device="cuda")
+        R.refine_step_ex(g, P, tu, te, -1, stats=stats, eos_written=eosw)
+        got = _np(g)
+        steps += 1
+        thr = np.where(cur[:, P:] == s.mask_id, tu, te)
+        ex = (info["margin"] <= margin) | (np.abs(info["conf"] - thr) <= MARGIN)
+        moved = got != cur
+        log(f"[tiny sharp ex step {step}] gpu moves {int(moved.sum())} (oracle {int((ref_next != cur).sum())}) "
+            f"checked {int((~ex).sum())}/{D} stats {_np(stats).tolist()}")
+        assert np.array_equal(got[:, :P], cur[:, :P])
+        assert np.array_equal(got[:, P:][~ex], ref_next[:, P:][~ex])
+        st = _np(stats).tolist()
+        assert st[0] == int(np.sum(moved & (cur == s.mask_id))) and st[1] == int(np.sum(moved & (cur != s.mask_id)))
+        assert int(_np(eosw)[0]) == 0
+        if step == 0:
+            first_written = got[:, P:][moved[:, P:] & ~ex]
+        traj.append(got.copy())
+        last_still = not moved.any()
+        if last_still:
+            break
+    assert first_written is not None and first_written.size > 0
+    d_draft = _cuda_i32(draft)
+    _, gst = R.refine_ex(_cuda_i32(prompt), d_draft, torch.tensor(mask, device="cuda"), w.n_steps, tu, te)
+    assert np.array_equal(_np(d_draft), traj[-1][:, P:])
+    assert gst["steps_run"] == steps
+    assert gst["stop_reason"] == (1 if last_still else 0)
+    # EOS: a token the first pass writes at a checked position ends the loop after pass 1
+    eos = int(first_written[0])
+    g1 = _cuda_i32(_tokens(w, s))
+    eosw = torch.zeros(1, dtype=torch.int32, device="cuda")
+    R.refine_step_ex(g1, P, tu, te, eos, eos_written=eosw)
+    n_eos = int(np.sum((_np(g1)[:, P:] == eos) & (_tokens(w, s)[:, P:] != eos)))
+    assert int(_np(eosw)[0]) == n_eos > 0
+    d2 = _cuda_i32(draft)
+    _, est = R.refine_ex(_cuda_i32(prompt), d2, torch.tensor(mask, device="cuda"), w.n_steps, tu, te, eos)
+    log(f"[tiny sharp ex] eos {eos}: {est}")
+    assert est["steps_run"] == 1 and est["stop_reason"] == 2
+    assert np.array_equal(_np(d2), traj[0][:, P:])
+
+
 @pytest.fixture(scope="module")
 def small():
     return _setup("small_moe")

@@ -341,6 +341,40 @@ def test_edit_rule_cases():
     assert new[0, 1] == 4
 
 
+def test_edit_rule_ex_cases():
+    """Two thresholds and the EOS count, worked by hand from the rule."""
+    from oracle.refine import edit_rule_ex
+    mask_id, eos = 9, 7
+    draft = np.array([[9, 3, 9, 4, 5]])
+    top1 = np.array([[2, 3, 9, 6, 7]])
+    conf = np.array([[0.5, 0.99, 0.99, 0.7, 0.95]])
+    # [MASK]->2 (0.5 >= 0.4); 3 unchanged (same token); [MASK] top-1 is [MASK]:
+    # stays; 4->6 refused (0.7 < 0.9); 5->7 (0.95 >= 0.9) writes the EOS id
+    new, unm, ed, ne = edit_rule_ex(draft, top1, conf, 0.4, 0.9, mask_id, eos)
+    assert new.tolist() == [[2, 3, 9, 4, 7]] and (unm, ed, ne) == (1, 1, 1)
+    # swapped thresholds: the unmask is refused (0.5 < 0.9), both edits pass
+    new, unm, ed, ne = edit_rule_ex(draft, top1, conf, 0.9, 0.4, mask_id, eos)
+    assert new.tolist() == [[9, 3, 9, 6, 7]] and (unm, ed, ne) == (0, 2, 1)
+    # eos disabled: no count; a slot already holding the EOS id is not "produced"
+    assert edit_rule_ex(draft, top1, conf, 0.4, 0.9, mask_id, -1)[3] == 0
+    d2 = np.array([[9, 3, 9, 4, 7]])
+    assert edit_rule_ex(d2, top1, conf, 0.4, 0.9, mask_id, eos)[3] == 0
+    # edit threshold > 1: only [MASK] slots move; unmask threshold > 1: only real tokens
+    rng = np.random.default_rng(3)
+    dr = rng.integers(0, 12, size=(4, 50))
+    t1 = rng.integers(0, 12, size=(4, 50))
+    cf = rng.random((4, 50))
+    n1 = edit_rule_ex(dr, t1, cf, 0.3, 1.5, 11)[0]
+    assert np.all((n1 == dr) | (dr == 11))
+    n2 = edit_rule_ex(dr, t1, cf, 1.5, 0.3, 11)[0]
+    assert np.all((n2 == dr) | (dr != 11))
+    # equal thresholds reduce to the single-threshold rule
+    for tau in (0.0, 0.3, 0.7, 1.1):
+        a = edit_rule_ex(dr, t1, cf, tau, tau, 11, -1)
+        b = edit_rule(dr, t1, cf, tau, 11)
+        assert np.array_equal(a[0], b[0]) and a[1:3] == b[1:3]
+
+
 # ---------------------------------------------------------------- composed step
 
 def test_identity_blocks_closed_form():
@@ -414,6 +448,31 @@ def test_refine_invariants(tiny):
     full, sf = refine(W, prompt, draft, mask, 3, tau)
     assert np.array_equal(ab, full)
     assert (ab == mid).sum() <= (a == mid).sum() <= mask.sum()
+
+
+def test_refine_ex_loop(tiny):
+    """Equal thresholds without EOS: the same run as refine (and stop_reason 1
+    or 0); with an EOS id that the first pass writes, the loop ends after that
+    pass (stop_reason 2) where the same run without EOS goes on."""
+    from oracle.refine import refine_ex
+    w, W = tiny
+    prompt, draft, mask = make_inputs(w)
+    P = w.prompt_len
+    t = np.concatenate([prompt, np.where(mask, w.model.mask_id, draft)], 1).astype(np.int32)
+    _, info = refine_step(W, t, P, 0.0)
+    tau = float(np.quantile(info["conf"], 0.5))
+    a, sa = refine(W, prompt, draft, mask, 3, tau)
+    b, sb = refine_ex(W, prompt, draft, mask, 3, tau, tau)
+    assert np.array_equal(a, b) and sa["steps_run"] == sb["steps_run"]
+    assert sb["stop_reason"] == (1 if sb["per_step"][-1]["n_unmasked"] + sb["per_step"][-1]["n_edited"] == 0 else 0)
+    # tau <= 0 makes pass 1 write every top-1: take one written token as EOS
+    t1, inf1 = refine_step(W, t, P, 0.0)
+    written = t1[:, P:][t1[:, P:] != t[:, P:]]
+    eos = int(written[0])
+    c, sc = refine_ex(W, prompt, draft, mask, 3, 0.0, 0.0, eos)
+    assert sc["steps_run"] == 1 and sc["stop_reason"] == 2 and np.array_equal(c, t1[:, P:])
+    d, sd = refine_ex(W, prompt, draft, mask, 3, 0.0, 0.0, -1)
+    assert sd["steps_run"] > 1 or sd["stop_reason"] == 1
 
 
 def test_layer_forward_collect_consistent(tiny):
