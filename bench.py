@@ -133,6 +133,41 @@ def cpu_baseline(w, layers_sample=1):
     }
 
 
+def bench_local(args, w, R, tokens0):
+    """Local refinement: a step is one pass over every chunk of the draft
+    (prompt ‖ chunk, the chunk at its positions in the full sequence)."""
+    import numpy as np
+    import torch
+    shape = w.model
+    B, P, D = w.batch, w.prompt_len, w.draft_len
+    L = min(args.local_span, D)
+    chunks = [(c0, torch.tensor(np.concatenate([tokens0[:, :P], tokens0[:, P + c0:P + min(c0 + L, D)]], 1),
+                                device="cuda")) for c0 in range(0, D, L)]
+
+    def one_step():
+        for c0, t in chunks:
+            R.refine_step_span(t, P, c0, w.threshold, w.threshold, workspace_draft_len=D)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        one_step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    flops = sum(step_flops(shape, B, P, t.shape[1] - P) for _, t in chunks)
+    print(json.dumps({
+        "metric": f"refined positions/sec per local refinement pass (chunks of {L})",
+        "value": B * D / (ms_step * 1e-3), "unit": "refined positions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "prompt_len": P, "draft_len": D, "local_span": L,
+                   "chunks": len(chunks)},
+        "step_mfma_frac": flops / (ms_step * 1e-3) / PEAK_BF16,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +177,8 @@ def main():
     ap.add_argument("--kernel", default="gemm_expert_gate_up", help="kernel reported in roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-table", action="store_true", help="also time every kernel (separate pass)")
+    ap.add_argument("--local-span", type=int, default=0,
+                    help="time local refinement instead: one pass over every draft chunk of this many tokens")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (reference for memory counters)")
     args = ap.parse_args()
@@ -179,6 +216,9 @@ def main():
     R.workspace(B, P, D)
     torch.cuda.synchronize()
 
+    if args.local_span:
+        bench_local(args, w, R, tokens0)
+        return
     for _ in range(args.warmup):
         R.refine_step(tokens, P, w.threshold)
     torch.cuda.synchronize()

@@ -182,6 +182,38 @@ dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_
                          void* hip_stream, dlm_stats* h_stats, int32_t* h_stop_reason);
 
 /*
+ * Local refinement (Sec. 6.3 / Table 10: refinement applied to 64-token
+ * chunks of the generated span instead of the whole span; App. D.4: staged
+ * schedules such as two passes at span 256 then two at 512).  Reading used
+ * here: a chunk is refined on its own, attending to the prompt and the chunk
+ * only, its tokens keeping their positions in the full sequence.
+ *
+ * dlm_refine_step_span: one pass over d_tokens [batch][prompt_len + span_len]
+ *   = prompt ‖ span, whose span token i sits at position prompt_len +
+ *   span_start + i (RoPE); otherwise as dlm_refine_step_ex.
+ * dlm_refine_local: for each stage g < n_stages (host arrays h_span, h_passes),
+ *   the draft is cut into chunks of h_span[g] tokens (the last may be shorter)
+ *   and each chunk gets up to h_passes[g] passes of dlm_refine_step_span,
+ *   stopping after a pass that changed nothing in it; the whole run ends after
+ *   a pass that wrote rule->eos_id (eos_id >= 0).  Slots with d_mask != 0
+ *   (may be NULL) start as mask_id; d_draft [batch][draft_len] is updated in
+ *   place.  The workspace is the one of (batch, prompt_len, draft_len).
+ *   h_stats: totals over all passes; h_stop_reason: 0 = some chunk used its
+ *   whole pass budget, 1 = every chunk stopped on a pass without change, 2 =
+ *   EOS written.  A schedule of one stage with span >= draft_len is
+ *   dlm_refine_ex.
+ */
+dlm_status dlm_refine_step_span(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t span_len,
+                                int32_t span_start, int32_t* d_tokens, const dlm_edit_rule* rule, void* d_workspace,
+                                size_t workspace_bytes, void* hip_stream, int32_t* d_top1, float* d_conf,
+                                dlm_stats* d_stats, int32_t* d_eos_written);
+dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                            const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_stages,
+                            const int32_t* h_span, const int32_t* h_passes, const dlm_edit_rule* rule,
+                            void* d_workspace, size_t workspace_bytes, void* hip_stream, dlm_stats* h_stats,
+                            int32_t* h_stop_reason);
+
+/*
  * Test hooks (same kernels as dlm_refine_step, intermediate results exposed).
  *
  * dlm_debug_forward: forward over d_tokens without the reduction; writes the

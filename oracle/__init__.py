@@ -9,6 +9,6 @@ CPU-baseline leg may import it.  It shares no code with the GPU library.
 from .weights import OracleWeights, philox4x32_10, tensor_id  # noqa: F401
 from .refine import (  # noqa: F401
     attention, edit_rule, edit_rule_ex, forward, layer_forward, layer_forward_rows, lm_head_reduce, moe_ffn, refine,
-    refine_ex, refine_step, refine_step_ex,
+    refine_ex, refine_local, refine_step, refine_step_ex,
     rms_norm, rope, route, softmax, swiglu,
 )

@@ -155,11 +155,12 @@ def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = True):
 
 # ---------------------------------------------------------------- forward
 
-def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True):
-    """One pre-norm block over x [B, S, d] (all positions, no attention mask)."""
+def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, positions: np.ndarray | None = None):
+    """One pre-norm block over x [B, S, d] (all positions, no attention mask);
+    positions [S] (default 0..S-1) are the RoPE positions of the S tokens."""
     B, S, d = x.shape
     H, KV, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
-    pos = np.arange(S)
+    pos = np.arange(S) if positions is None else np.asarray(positions)
     x = x.astype(F64, copy=True)
     info = {"route_gap": None, "route_ids": None}
     attn = np.empty((B, S, H * hd), dtype=F64)
@@ -210,10 +211,12 @@ def layer_forward_rows(shape, L: dict, x_seq: np.ndarray, rows: np.ndarray, deci
     return x, info
 
 
-def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = True):
+def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = True,
+            positions: np.ndarray | None = None):
     """Residual stream after the last layer (before the final norm): [B, S, d].
 
-    With collect=True also returns per-layer infos and per-layer inputs.
+    With collect=True also returns per-layer infos and per-layer inputs;
+    positions as in layer_forward.
     """
     shape = W.shape
     x = W.embed_rows(np.asarray(tokens)).astype(F64)
@@ -221,7 +224,7 @@ def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = Tr
     for l in range(shape.n_layers):
         if collect:
             inputs.append(x.copy())
-        x, info = layer_forward(shape, W.layer(l), x, decide_bf16)
+        x, info = layer_forward(shape, W.layer(l), x, decide_bf16, positions)
         infos.append(info)
     if collect:
         return x, infos, inputs
@@ -287,11 +290,11 @@ def edit_rule(draft: np.ndarray, top1: np.ndarray, conf: np.ndarray, tau: float,
     return new, n_unmasked, n_edited
 
 
-def _reduce_draft(W, tokens: np.ndarray, prompt_len: int, decide_bf16: bool):
+def _reduce_draft(W, tokens: np.ndarray, prompt_len: int, decide_bf16: bool, positions: np.ndarray | None = None):
     """Forward over the whole sequence, then top-1 and confidence of every draft position."""
     B, S = tokens.shape
     D = S - prompt_len
-    x = forward(W, tokens, decide_bf16=decide_bf16)
+    x = forward(W, tokens, decide_bf16=decide_bf16, positions=positions)
     red = lm_head_reduce(W, x[:, prompt_len:, :].reshape(B * D, -1), decide_bf16=decide_bf16)
     return {"top1": red["top1"].reshape(B, D), "conf": red["conf"].reshape(B, D),
             "max_logit": red["max_logit"].reshape(B, D), "margin": red["margin"].reshape(B, D)}
@@ -329,9 +332,15 @@ def edit_rule_ex(draft: np.ndarray, top1: np.ndarray, conf: np.ndarray, tau_unma
 
 
 def refine_step_ex(W, tokens: np.ndarray, prompt_len: int, tau_unmask: float, tau_edit: float, eos_id: int = -1,
-                   decide_bf16: bool = True):
-    """One refinement pass under edit_rule_ex."""
-    info = _reduce_draft(W, tokens, prompt_len, decide_bf16)
+                   decide_bf16: bool = True, span_start: int = 0):
+    """One refinement pass under edit_rule_ex.  With span_start, the draft part
+    of tokens is a span of a longer draft: its token i sits at position
+    prompt_len + span_start + i."""
+    S = tokens.shape[1]
+    positions = None
+    if span_start:
+        positions = np.concatenate([np.arange(prompt_len), prompt_len + span_start + np.arange(S - prompt_len)])
+    info = _reduce_draft(W, tokens, prompt_len, decide_bf16, positions)
     new_draft, n_unm, n_edit, n_eos = edit_rule_ex(tokens[:, prompt_len:], info["top1"], info["conf"],
                                                    tau_unmask, tau_edit, W.shape.mask_id, eos_id)
     out = tokens.copy()
@@ -366,6 +375,55 @@ def refine_ex(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None,
             break
     stats["n_masked_left"] = int(np.sum(tokens[:, P:] == shape.mask_id))
     return tokens[:, P:].copy(), stats
+
+
+def refine_local(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, schedule,
+                 tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = True):
+    """Local / staged refinement (Sec. 6.3 and Table 10: refinement in 64-token
+    chunks of the generated span; App. D.4: staged schedules of span sizes).
+    Reading used here: for each stage (span, passes) of the schedule, the draft
+    is cut into chunks of `span` tokens (the last may be shorter); a chunk is
+    refined on its own -- the sequence is prompt ‖ chunk, the chunk's tokens at
+    their positions in the full sequence -- for up to `passes` passes of
+    refine_step_ex, stopping after a pass that changed nothing in it; a pass
+    that writes eos_id (eos_id >= 0) ends the whole run.  stop_reason: 0 some
+    chunk used its whole budget, 1 every chunk stopped without change, 2 EOS."""
+    shape = W.shape
+    P = prompt.shape[1]
+    D = draft.shape[1]
+    d = draft.copy()
+    if mask is not None:
+        d[mask] = shape.mask_id
+    stats = {"steps_run": 0, "n_unmasked": 0, "n_edited": 0, "stop_reason": 1, "chunks": []}
+    eos_stop = False
+    for span, passes in schedule:
+        L = min(int(span), D)
+        for c0 in range(0, D, L):
+            if eos_stop:
+                break
+            tokens = np.concatenate([prompt, d[:, c0:c0 + L]], axis=1).astype(np.int32)
+            still = False
+            for _ in range(passes):
+                tokens, info = refine_step_ex(W, tokens, P, tau_unmask, tau_edit, eos_id, decide_bf16, span_start=c0)
+                stats["steps_run"] += 1
+                stats["n_unmasked"] += info["n_unmasked"]
+                stats["n_edited"] += info["n_edited"]
+                if info["n_unmasked"] + info["n_edited"] == 0:
+                    still = True
+                    break
+                if eos_id >= 0 and info["n_eos"] > 0:
+                    eos_stop = True
+                    break
+            if not still and passes > 0 and stats["stop_reason"] != 2:
+                stats["stop_reason"] = 0
+            d[:, c0:c0 + L] = tokens[:, P:]
+            stats["chunks"].append((c0, L))
+        if eos_stop:
+            break
+    if eos_stop:
+        stats["stop_reason"] = 2
+    stats["n_masked_left"] = int(np.sum(d == shape.mask_id))
+    return d, stats
 
 
 def refine(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_steps: int,

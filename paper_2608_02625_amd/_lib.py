@@ -57,6 +57,10 @@ SIGNATURES = [
     ("dlm_refine_step_ex", _I, [_P, _I, _I, _I, _P, ctypes.POINTER(DlmEditRule), _P, _SZ, _P, _P, _P, _P, _P]),
     ("dlm_refine_ex", _I, [_P, _I, _I, _I, _P, _P, _P, _I, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
                            ctypes.POINTER(DlmStats), ctypes.POINTER(_I)]),
+    ("dlm_refine_step_span", _I, [_P, _I, _I, _I, _I, _P, ctypes.POINTER(DlmEditRule), _P, _SZ, _P, _P, _P, _P,
+                                  _P]),
+    ("dlm_refine_local", _I, [_P, _I, _I, _I, _P, _P, _P, _I, _P, _P, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
+                              ctypes.POINTER(DlmStats), ctypes.POINTER(_I)]),
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
     ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),

@@ -118,6 +118,28 @@ __global__ void edit_kernel(int32_t* __restrict__ tokens, int S, int P, int D,
     }
 }
 
+__global__ void span_gather_kernel(const int32_t* __restrict__ prompt, const int32_t* __restrict__ draft,
+                                   int32_t* __restrict__ tokens, int P, int D, int c0, int L, int n) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n) return;
+    const int S = P + L;
+    const int b = idx / S, s = idx - b * S;
+    tokens[idx] = s < P ? prompt[(int64_t)b * P + s] : draft[(int64_t)b * D + c0 + (s - P)];
+}
+
+__global__ void span_scatter_kernel(const int32_t* __restrict__ tokens, int32_t* __restrict__ draft, int P, int D,
+                                    int c0, int L, int n) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n) return;
+    const int b = idx / L, i = idx - b * L;
+    draft[(int64_t)b * D + c0 + i] = tokens[(int64_t)b * (P + L) + P + i];
+}
+
+__global__ void mask_draft_kernel(int32_t* __restrict__ draft, const uint8_t* __restrict__ mask, int n, int mask_id) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx < n && mask[idx]) draft[idx] = mask_id;
+}
+
 __global__ void apply_mask_kernel(const int32_t* __restrict__ prompt, const int32_t* __restrict__ draft,
                                   const uint8_t* __restrict__ mask, int32_t* __restrict__ tokens,
                                   int P, int D, int mask_id, int n) {
@@ -197,6 +219,22 @@ void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top
     const int n = B * D;
     hipLaunchKernelGGL(edit_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, S, P, D, top1,
                        conf, thr_unmask, thr_edit, mask_id, eos_id, counters, eos_count, out_top1, out_conf, n);
+}
+
+void launch_span_gather(const int32_t* prompt, const int32_t* draft, int32_t* tokens, int B, int P, int D,
+                        int c0, int L, hipStream_t st) {
+    const int n = B * (P + L);
+    hipLaunchKernelGGL(span_gather_kernel, dim3((n + 255) / 256), dim3(256), 0, st, prompt, draft, tokens, P, D, c0,
+                       L, n);
+}
+
+void launch_span_scatter(const int32_t* tokens, int32_t* draft, int B, int P, int D, int c0, int L, hipStream_t st) {
+    const int n = B * L;
+    hipLaunchKernelGGL(span_scatter_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, draft, P, D, c0, L, n);
+}
+
+void launch_mask_draft(int32_t* draft, const uint8_t* mask, int n, int mask_id, hipStream_t st) {
+    hipLaunchKernelGGL(mask_draft_kernel, dim3((n + 255) / 256), dim3(256), 0, st, draft, mask, n, mask_id);
 }
 
 void launch_apply_mask(const int32_t* prompt, const int32_t* draft, const uint8_t* mask,

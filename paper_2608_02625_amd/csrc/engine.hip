@@ -252,6 +252,7 @@ struct Ctx {
     hipStream_t st;
     int B, P, D, S, T, R;
     bool h_ready = false;           // h already holds the next block's normalised input
+    int pos_shift = 0;              // draft positions are P + shift + i (a span refined on its own)
     template <class Tp>
     Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
     const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
@@ -432,7 +433,8 @@ dlm_status run_layer(Ctx& x, int l) {
 
 dlm_status run_prologue(Ctx& x, const int32_t* tokens) {
     const dlm_config& c = x.c;
-    LAUNCH(x, "rope_table", launch_rope_table(x.at<float2>(x.w.rope), x.S, c.head_dim / 2, (double)c.rope_theta, x.st));
+    LAUNCH(x, "rope_table", launch_rope_table(x.at<float2>(x.w.rope), x.S, c.head_dim / 2, (double)c.rope_theta, x.P,
+                                              x.pos_shift, x.st));
     LAUNCH(x, "vt_pad_zero", launch_vt_pad_zero(x.at<bf16_t>(x.w.v), (int64_t)x.B * c.n_kv_heads * c.head_dim, x.S, x.st));
     if (tokens) LAUNCH(x, "embed", launch_embed(tokens, x.wt(x.m->plan.emb), x.at<float>(x.w.x), x.T, c.d_model, c.vocab, x.st));
     return DLM_OK;
@@ -611,6 +613,88 @@ dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_
     HIP_TRY(hipMemcpyAsync(&st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
     HIP_TRY(hipStreamSynchronize(x.st));
     tot.n_masked_left = st.n_masked_left;
+    if (h_stats) *h_stats = tot;
+    if (h_stop_reason) *h_stop_reason = reason;
+    return DLM_OK;
+}
+
+dlm_status dlm_refine_step_span(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t span_len,
+                                int32_t span_start, int32_t* d_tokens, const dlm_edit_rule* rule, void* d_workspace,
+                                size_t workspace_bytes, void* hip_stream, int32_t* d_top1, float* d_conf,
+                                dlm_stats* d_stats, int32_t* d_eos_written) {
+    Workspace w;
+    TRY(check_common(m, batch, prompt_len, span_len, d_workspace, workspace_bytes, &w));
+    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+    if (span_start < 0) return fail(DLM_ERR_INVALID_ARG, "span_start < 0");
+    TRY(check_rule(m->cfg, rule));
+    Ctx x = ctx_for(m, batch, prompt_len, span_len, d_workspace, w, hip_stream);
+    x.pos_shift = span_start;
+    return step_impl(x, d_tokens, *rule, d_top1, d_conf, d_stats, d_eos_written);
+}
+
+dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                            const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_stages,
+                            const int32_t* h_span, const int32_t* h_passes, const dlm_edit_rule* rule,
+                            void* d_workspace, size_t workspace_bytes, void* hip_stream, dlm_stats* h_stats,
+                            int32_t* h_stop_reason) {
+    Workspace wfull;
+    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &wfull));
+    if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
+    if (n_stages < 0 || (n_stages > 0 && (!h_span || !h_passes))) return fail(DLM_ERR_INVALID_ARG, "bad schedule");
+    for (int i = 0; i < n_stages; ++i)
+        if (h_span[i] < 1 || h_passes[i] < 0) return fail(DLM_ERR_INVALID_ARG, "span < 1 or passes < 0");
+    TRY(check_rule(m->cfg, rule));
+    hipStream_t st = (hipStream_t)hip_stream;
+    const int n = batch * draft_len;
+    if (d_mask) launch_mask_draft(d_draft, d_mask, n, m->cfg.mask_id, st);
+    HIP_TRY(hipGetLastError());
+    dlm_stats tot{0, 0, 0, 0};
+    int32_t reason = 1;                                // every chunk stopped on its own (or nothing ran)
+    bool eos_stop = false;
+    for (int g = 0; g < n_stages && !eos_stop; ++g) {
+        const int L = std::min<int>(h_span[g], draft_len);
+        for (int c0 = 0; c0 < draft_len && !eos_stop; c0 += L) {
+            const int len = std::min(L, draft_len - c0);
+            Workspace w;
+            TRY(check_common(m, batch, prompt_len, len, d_workspace, workspace_bytes, &w));
+            Ctx x = ctx_for(m, batch, prompt_len, len, d_workspace, w, hip_stream);
+            x.pos_shift = c0;
+            int32_t* tokens = x.at<int32_t>(w.tokens);
+            int32_t* counters = x.at<int32_t>(w.counters);
+            launch_span_gather(d_prompt, d_draft, tokens, batch, prompt_len, draft_len, c0, len, st);
+            HIP_TRY(hipGetLastError());
+            bool still = false;
+            for (int p = 0; p < h_passes[g]; ++p) {
+                TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
+                int32_t c[5] = {};
+                HIP_TRY(hipMemcpyAsync(c, counters, sizeof(c), hipMemcpyDeviceToHost, st));
+                HIP_TRY(hipStreamSynchronize(st));
+                tot.n_unmasked += c[0];
+                tot.n_edited += c[1];
+                tot.steps_run += 1;
+                if (c[0] + c[1] == 0) {
+                    still = true;
+                    break;
+                }
+                if (rule->eos_id >= 0 && c[4] > 0) {
+                    eos_stop = true;
+                    break;
+                }
+            }
+            if (!still && h_passes[g] > 0) reason = reason == 2 ? 2 : 0;
+            launch_span_scatter(tokens, d_draft, batch, prompt_len, draft_len, c0, len, st);
+            HIP_TRY(hipGetLastError());
+        }
+    }
+    if (eos_stop) reason = 2;
+    int32_t* counters = reinterpret_cast<int32_t*>((char*)d_workspace + wfull.counters);
+    launch_zero_i32(counters, 4, st);
+    launch_count_masks(d_draft, batch, draft_len, 0, draft_len, m->cfg.mask_id, counters + 2, st);
+    HIP_TRY(hipGetLastError());
+    dlm_stats fin{};
+    HIP_TRY(hipMemcpyAsync(&fin, counters, sizeof(fin), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    tot.n_masked_left = fin.n_masked_left;
     if (h_stats) *h_stats = tot;
     if (h_stop_reason) *h_stop_reason = reason;
     return DLM_OK;

@@ -82,11 +82,14 @@ __global__ void fill_bf16_kernel(bf16_t* __restrict__ dst, uint64_t n, bf16_t v)
 }
 
 // cos/sin table [S][half] for rotate-half RoPE, angle = pos * theta^(-2i/hd),
-// evaluated in double and rounded to float.
-__global__ void rope_table_kernel(float2* __restrict__ tab, int S, int half, double theta) {
+// evaluated in double and rounded to float.  Row s holds position s for the
+// first P rows and s + shift after them (a draft span refined on its own keeps
+// its positions in the full sequence).
+__global__ void rope_table_kernel(float2* __restrict__ tab, int S, int half, double theta, int P, int shift) {
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= S * half) return;
-    const int pos = idx / half, i = idx % half;
+    const int row = idx / half, i = idx % half;
+    const int pos = row < P ? row : row + shift;
     const double inv = pow(theta, -2.0 * (double)i / (double)(2 * half));
     double s, c;
     sincos((double)pos * inv, &s, &c);
@@ -107,7 +110,7 @@ void launch_fill_bf16(bf16_t* dst, uint64_t n, bf16_t v, hipStream_t st) {
     hipLaunchKernelGGL(fill_bf16_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dst, n, v);
 }
 
-void launch_rope_table(float2* tab, int S, int half, double theta, hipStream_t st) {
+void launch_rope_table(float2* tab, int S, int half, double theta, int P, int shift, hipStream_t st) {
     const int n = S * half;
-    hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tab, S, half, theta);
+    hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tab, S, half, theta, P, shift);
 }

@@ -10,7 +10,8 @@ typedef uint16_t bf16_t;
 void launch_init_weights(bf16_t* dst, uint64_t n_phys, uint32_t cols, uint32_t tid_a,
                          uint32_t tid_b, int layout, uint64_t seed, float c, hipStream_t st);
 void launch_fill_bf16(bf16_t* dst, uint64_t n, bf16_t v, hipStream_t st);
-void launch_rope_table(float2* tab, int S, int half, double theta, hipStream_t st);
+// RoPE (cos, sin) table [S][half]; rows >= P take position row + shift.
+void launch_rope_table(float2* tab, int S, int half, double theta, int P, int shift, hipStream_t st);
 
 // V is kept transposed for attention: V^T [B][KV][hd][S64], S64 = S rounded up
 // to the 64-key attention tile.  Inside each aligned group of 16 keys the keys
@@ -87,6 +88,12 @@ void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top
                  int32_t* eos_count, int32_t* out_top1, float* out_conf, hipStream_t st);
 void launch_apply_mask(const int32_t* prompt, const int32_t* draft, const uint8_t* mask,
                        int32_t* tokens, int B, int P, int D, int mask_id, hipStream_t st);
+// Draft spans refined on their own: tokens [B][P + L] = prompt ‖ draft[:, c0 : c0 + L]
+// (draft rows of D), and back; mask_id into the masked slots of the draft.
+void launch_span_gather(const int32_t* prompt, const int32_t* draft, int32_t* tokens, int B, int P, int D,
+                        int c0, int L, hipStream_t st);
+void launch_span_scatter(const int32_t* tokens, int32_t* draft, int B, int P, int D, int c0, int L, hipStream_t st);
+void launch_mask_draft(int32_t* draft, const uint8_t* mask, int n, int mask_id, hipStream_t st);
 void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, int P, int D,
                            hipStream_t st);
 void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int mask_id,

@@ -142,6 +142,45 @@ class Refiner:
         out["stop_reason"] = int(reason.value)
         return draft, out
 
+    def refine_step_span(self, tokens: torch.Tensor, prompt_len: int, span_start: int, unmask_threshold: float,
+                         edit_threshold: float, eos_id: int = -1, workspace_draft_len: int | None = None,
+                         top1: torch.Tensor | None = None, conf: torch.Tensor | None = None,
+                         stats: torch.Tensor | None = None, eos_written: torch.Tensor | None = None):
+        """One pass over prompt ‖ span (int32 [B, P + L], in place), span token i at position P + span_start + i."""
+        B, S = tokens.shape
+        L = S - prompt_len
+        ws = self.workspace(B, prompt_len, L if workspace_draft_len is None else workspace_draft_len)
+        rule = _lib.DlmEditRule(float(unmask_threshold), float(edit_threshold), int(eos_id))
+        check(self.lib.dlm_refine_step_span(self._handle, B, prompt_len, L, int(span_start), tokens.data_ptr(),
+                                            ctypes.byref(rule), ws.data_ptr(), ws.numel(), self.stream, _ptr(top1),
+                                            _ptr(conf), _ptr(stats), _ptr(eos_written)), "dlm_refine_step_span")
+        return tokens
+
+    def refine_local(self, prompt: torch.Tensor, draft: torch.Tensor, mask: torch.Tensor | None,
+                     schedule: list[tuple[int, int]], unmask_threshold: float, edit_threshold: float,
+                     eos_id: int = -1):
+        """Local / staged refinement: schedule = [(span, passes), ...] (draft int32 [B, D], in place)."""
+        B, P = prompt.shape
+        D = draft.shape[1]
+        ws = self.workspace(B, P, D)
+        m = None
+        if mask is not None:
+            m = mask.to(torch.uint8).contiguous()
+        n = len(schedule)
+        spans = (ctypes.c_int32 * max(n, 1))(*[int(a) for a, _ in schedule])
+        passes = (ctypes.c_int32 * max(n, 1))(*[int(b) for _, b in schedule])
+        st = DlmStats()
+        reason = ctypes.c_int32(-1)
+        rule = _lib.DlmEditRule(float(unmask_threshold), float(edit_threshold), int(eos_id))
+        check(self.lib.dlm_refine_local(self._handle, B, P, D, prompt.data_ptr() if P else None, draft.data_ptr(),
+                                        _ptr(m), n, ctypes.cast(spans, ctypes.c_void_p),
+                                        ctypes.cast(passes, ctypes.c_void_p), ctypes.byref(rule), ws.data_ptr(),
+                                        ws.numel(), self.stream, ctypes.byref(st), ctypes.byref(reason)),
+              "dlm_refine_local")
+        out = st.as_dict()
+        out["stop_reason"] = int(reason.value)
+        return draft, out
+
     # -------------------------------------------------------------- test hooks
     def debug_forward(self, tokens: torch.Tensor, prompt_len: int, want_logits: bool = False):
         B, S = tokens.shape

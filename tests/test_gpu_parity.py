@@ -245,6 +245,54 @@ def test_refine_ex_two_thresholds_and_eos(tiny_sharp):
     assert np.array_equal(_np(d2), traj[0][:, P:])
 
 
+def test_refine_local_schedule(tiny_sharp):
+    """Local / staged refinement, schedule 2 passes at span 32 then 2 at span 64
+    (a chunk refined on its own with its positions in the full sequence):
+    along the GPU's own trajectory every pass agrees with the oracle's pass on
+    the same chunk input at non-exempt positions, and the loop entry point
+    reproduces the trajectory exactly."""
+    import oracle
+    torch = _torch()
+    w, s, R, W = tiny_sharp
+    prompt, draft, mask = make_inputs(w)
+    P, D = w.prompt_len, w.draft_len
+    margin = MARGIN * s.lm_head_scale
+    _, info0 = oracle.refine_step(W, _tokens(w, s), P, 1.0)
+    tu, te = (float(np.round(np.quantile(info0["conf"], q), 2)) for q in (0.6, 0.85))
+    schedule = [(32, 2), (64, 2)]
+    cur_draft = np.where(mask, s.mask_id, draft).astype(np.int32)
+    steps, checked, reason = 0, 0, 1
+    for span, passes in schedule:
+        for c0 in range(0, D, span):
+            L = min(span, D - c0)
+            g = _cuda_i32(np.concatenate([prompt, cur_draft[:, c0:c0 + L]], 1))
+            still = False
+            for _ in range(passes):
+                cur = _np(g).copy()
+                ref_next, info = oracle.refine_step_ex(W, cur, P, tu, te, span_start=c0)
+                R.refine_step_span(g, P, c0, tu, te, workspace_draft_len=D)
+                got = _np(g)
+                steps += 1
+                thr = np.where(cur[:, P:] == s.mask_id, tu, te)
+                ex = (info["margin"] <= margin) | (np.abs(info["conf"] - thr) <= MARGIN)
+                checked += int((~ex).sum())
+                assert np.array_equal(got[:, :P], cur[:, :P])
+                assert np.array_equal(got[:, P:][~ex], ref_next[:, P:][~ex])
+                if not (got != cur).any():
+                    still = True
+                    break
+            if not still:
+                reason = 0
+            cur_draft[:, c0:c0 + L] = _np(g)[:, P:]
+    log(f"[tiny sharp local] {steps} passes, {checked} decisions checked, reason {reason}")
+    assert checked > 0
+    d_draft = _cuda_i32(draft)
+    _, st = R.refine_local(_cuda_i32(prompt), d_draft, torch.tensor(mask, device="cuda"), schedule, tu, te)
+    assert np.array_equal(_np(d_draft), cur_draft)
+    assert st["steps_run"] == steps and st["stop_reason"] == reason
+    assert st["n_masked_left"] == int(np.sum(cur_draft == s.mask_id))
+
+
 @pytest.fixture(scope="module")
 def small():
     return _setup("small_moe")

@@ -475,6 +475,48 @@ def test_refine_ex_loop(tiny):
     assert sd["steps_run"] > 1 or sd["stop_reason"] == 1
 
 
+def test_rope_positions_in_forward(tiny):
+    """Shifting every position by the same amount leaves the forward unchanged
+    (RoPE scores depend on offsets only); shifting only the draft positions
+    changes it (the positions reach the blocks)."""
+    w, W = tiny
+    prompt, draft, _ = make_inputs(w)
+    t = np.concatenate([prompt, draft], 1)
+    S = t.shape[1]
+    base = forward(W, t)
+    np.testing.assert_allclose(forward(W, t, positions=np.arange(S) + 37), base, rtol=0, atol=1e-9)
+    shifted = np.concatenate([np.arange(w.prompt_len), w.prompt_len + 16 + np.arange(S - w.prompt_len)])
+    assert np.abs(forward(W, t, positions=shifted) - base).max() > 1e-6
+
+
+def test_refine_local_schedules(tiny):
+    """One stage spanning the draft is refine_ex; with an empty prompt each
+    chunk equals refine_ex of the chunk alone (positions enter through offsets
+    only); a chunk's result does not depend on the other chunks."""
+    from oracle.refine import refine_ex, refine_local
+    w, W = tiny
+    prompt, draft, mask = make_inputs(w)
+    P, D = w.prompt_len, w.draft_len
+    t = np.concatenate([prompt, np.where(mask, w.model.mask_id, draft)], 1).astype(np.int32)
+    _, info = refine_step(W, t, P, 0.0)
+    tau = float(np.quantile(info["conf"], 0.5))
+    a, sa = refine_local(W, prompt, draft, mask, [(D, 3)], tau, tau)
+    b, sb = refine_ex(W, prompt, draft, mask, 3, tau, tau)
+    assert np.array_equal(a, b) and sa["steps_run"] == sb["steps_run"] and sa["stop_reason"] == sb["stop_reason"]
+    # empty prompt, two chunks of 32: chunk c alone at positions 0..31
+    empty = np.zeros((1, 0), dtype=prompt.dtype)
+    c, sc = refine_local(W, empty, draft, mask, [(32, 2)], 0.0, 0.0)
+    for c0 in (0, 32):
+        alone, _ = refine_ex(W, empty, draft[:, c0:c0 + 32], mask[:, c0:c0 + 32], 2, 0.0, 0.0)
+        assert np.array_equal(c[:, c0:c0 + 32], alone)
+    # chunk independence: changing the second chunk leaves the first one's result
+    d2 = draft.copy()
+    d2[:, 40:] = (d2[:, 40:] + 1) % (w.model.vocab - 1)
+    e, _ = refine_local(W, prompt, d2, mask, [(32, 2)], 0.0, 0.0)
+    f, _ = refine_local(W, prompt, draft, mask, [(32, 2)], 0.0, 0.0)
+    assert np.array_equal(e[:, :32], f[:, :32]) and not np.array_equal(e[:, 32:], f[:, 32:])
+
+
 def test_layer_forward_collect_consistent(tiny):
     w, W = tiny
     prompt, draft, _ = make_inputs(w)
