@@ -2,7 +2,7 @@
 
 Plain float64 NumPy (plus a small C weight generator) implementation of one
 refinement step and of the refine loop, written from the paper's description
-(Sec. 4.2, App. C.4).  Only tests/, the smoke check and the benchmark's
+(Sec. 4.2, App. C.4), and of block-AR drafting (Sec. 3.3, Sec. 4.1).  Only tests/, the smoke check and the benchmark's
 CPU-baseline leg may import it.  It shares no code with the GPU library.
 """
 
@@ -12,3 +12,4 @@ from .refine import (  # noqa: F401
     refine_ex, refine_local, refine_step, refine_step_ex,
     rms_norm, rope, route, softmax, swiglu,
 )
+from .draft import block_key_limit, draft, draft_forward_block, draft_select, draft_step  # noqa: F401

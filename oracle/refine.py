@@ -83,20 +83,27 @@ def softmax(z: np.ndarray, axis: int = -1) -> np.ndarray:
     return e / np.sum(e, axis=axis, keepdims=True)
 
 
-def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, key_limit: np.ndarray | None = None) -> np.ndarray:
     """Non-causal attention: every query attends to all S keys.
 
     q: [S, H, hd]; k, v: [S, KV, hd] with H a multiple of KV (query head h reads
-    key/value head h // (H // KV)).  Returns [S, H, hd].
+    key/value head h // (H // KV)).  Returns [S, H, hd].  With key_limit [S],
+    query i attends to keys 0 .. key_limit[i]-1 only (the block-causal mask of
+    block-AR drafting, Sec. 3.3); the refiner passes none.
     """
     S, H, hd = q.shape
     KV = k.shape[1]
     group = H // KV
     out = np.empty((S, H, hd), dtype=F64)
     scale = 1.0 / np.sqrt(hd)
+    allowed = None
+    if key_limit is not None:
+        allowed = np.arange(k.shape[0])[None, :] < np.asarray(key_limit)[:, None]
     for h in range(H):
         kv = h // group
         scores = (q[:, h, :] @ k[:, kv, :].T) * scale                 # [S, S]
+        if allowed is not None:
+            scores = np.where(allowed, scores, -np.inf)
         out[:, h, :] = softmax(scores, axis=-1) @ v[:, kv, :]
     return out
 
@@ -155,9 +162,11 @@ def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = True):
 
 # ---------------------------------------------------------------- forward
 
-def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, positions: np.ndarray | None = None):
-    """One pre-norm block over x [B, S, d] (all positions, no attention mask);
-    positions [S] (default 0..S-1) are the RoPE positions of the S tokens."""
+def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, positions: np.ndarray | None = None,
+                  key_limit: np.ndarray | None = None):
+    """One pre-norm block over x [B, S, d] (all positions; no attention mask
+    unless key_limit [S] is given, see attention); positions [S] (default
+    0..S-1) are the RoPE positions of the S tokens."""
     B, S, d = x.shape
     H, KV, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
     pos = np.arange(S) if positions is None else np.asarray(positions)
@@ -171,7 +180,7 @@ def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, posit
         v = (h @ L["wv"].astype(F64).T).reshape(S, KV, hd)
         q = rope(q, pos, shape.rope_theta)
         kk = rope(kk, pos, shape.rope_theta)
-        attn[b] = attention(q, kk, v).reshape(S, H * hd)
+        attn[b] = attention(q, kk, v, key_limit).reshape(S, H * hd)
     x += attn @ L["wo"].astype(F64).T
     h2 = rms_norm(x.reshape(B * S, d), L["g2"], shape.norm_eps)
     if shape.n_experts == 0:
@@ -212,11 +221,11 @@ def layer_forward_rows(shape, L: dict, x_seq: np.ndarray, rows: np.ndarray, deci
 
 
 def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = True,
-            positions: np.ndarray | None = None):
+            positions: np.ndarray | None = None, key_limit: np.ndarray | None = None):
     """Residual stream after the last layer (before the final norm): [B, S, d].
 
     With collect=True also returns per-layer infos and per-layer inputs;
-    positions as in layer_forward.
+    positions and key_limit as in layer_forward.
     """
     shape = W.shape
     x = W.embed_rows(np.asarray(tokens)).astype(F64)
@@ -224,7 +233,7 @@ def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = Tr
     for l in range(shape.n_layers):
         if collect:
             inputs.append(x.copy())
-        x, info = layer_forward(shape, W.layer(l), x, decide_bf16, positions)
+        x, info = layer_forward(shape, W.layer(l), x, decide_bf16, positions, key_limit)
         infos.append(info)
     if collect:
         return x, infos, inputs
