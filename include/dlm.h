@@ -214,6 +214,63 @@ dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int
                             int32_t* h_stop_reason);
 
 /*
+ * Block-AR drafting (Sec. 3.3 Block Autoregressive Diffusion, Sec. 4.1
+ * Drafting; the b/s/t settings of Table 9 and Table 10: block size, steps per
+ * block, confidence threshold).
+ *
+ * The draft_len response positions after the prompt are cut into blocks of
+ * block_len (1..1024; the last block may be shorter), generated in order.
+ * Visibility is block-causal: a position of block k attends to the prompt,
+ * to blocks 0..k-1 and to its own block; the prompt attends to itself.  K and
+ * V of the prompt and of finished blocks are computed once, from their final
+ * tokens, and kept per layer in the workspace.  Each block starts all
+ * [MASK]; one step is a forward of the block's rows followed by the
+ * unmasking: with n masked slots in the block (per sequence) and r steps left
+ * for it, quota = ceil(n / r); every masked slot whose confidence (softmax
+ * probability of its top-1) is >= threshold takes its top-1, or, when those
+ * are fewer than the quota, the quota most confident masked slots do (equal
+ * confidences: lower position first).  Drafting never changes a real token.
+ * A block ends once no sequence of the batch has a [MASK] in it, at the
+ * latest after steps_per_block steps.
+ *
+ * dlm_draft_workspace_bytes: device workspace size for the drafting entry
+ *   points at (batch, prompt_len, draft_len, block_len); 0 for an invalid
+ *   shape.  It holds the per-layer K/V caches of all prompt_len + draft_len
+ *   positions.
+ * dlm_draft: d_prompt int32 [batch][prompt_len] (may be NULL when prompt_len
+ *   is 0), d_draft int32 [batch][draft_len] (output; every slot is
+ *   written).  h_stats (host, may be NULL): n_unmasked = slots given a real
+ *   token, n_edited = 0, n_masked_left = [MASK] slots left in the draft (a
+ *   step may select a slot whose top-1 is mask_id itself), steps_run = steps
+ *   over all blocks.  h_block_steps (host, may be NULL): steps of each block,
+ *   ceil(draft_len / block_len) entries.  Synchronises the stream once per
+ *   step (the block's stop test) and returns when the draft is written.
+ * dlm_draft_step: one step on block block_index of d_tokens int32
+ *   [batch][prompt_len + draft_len] (prompt, finished blocks, the block in
+ *   progress; later positions are not read), with steps_left (>= 1) steps
+ *   left for the block; the K/V of the prompt and of the earlier blocks are
+ *   computed from d_tokens first.  The block's slots are updated in place;
+ *   d_top1 / d_conf / d_max_logit (device, may be NULL) receive the top-1,
+ *   its confidence and the max logit of the block's rows [batch][block rows]
+ *   (before the update); d_stats (device, may be NULL):
+ *   n_unmasked, n_edited = 0, n_masked_left in the block, steps_run = 1.
+ *   Asynchronous on hip_stream.
+ * Errors: NULL handle / buffers, block_len outside 1..1024, steps < 1,
+ * block_index out of range, NaN threshold -> DLM_ERR_INVALID_ARG; workspace
+ * too small -> DLM_ERR_WORKSPACE.  Token ids must lie in [0, vocab).
+ */
+size_t dlm_draft_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                                 int32_t block_len);
+dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, const int32_t* d_prompt,
+                     int32_t* d_draft, int32_t block_len, int32_t steps_per_block, float threshold,
+                     void* d_workspace, size_t workspace_bytes, void* hip_stream, dlm_stats* h_stats,
+                     int32_t* h_block_steps);
+dlm_status dlm_draft_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, int32_t block_len,
+                          int32_t block_index, int32_t steps_left, float threshold, int32_t* d_tokens,
+                          void* d_workspace, size_t workspace_bytes, void* hip_stream, int32_t* d_top1,
+                          float* d_conf, float* d_max_logit, dlm_stats* d_stats);
+
+/*
  * Test hooks (same kernels as dlm_refine_step, intermediate results exposed).
  *
  * dlm_debug_forward: forward over d_tokens without the reduction; writes the

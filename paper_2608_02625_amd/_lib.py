@@ -61,6 +61,10 @@ SIGNATURES = [
                                   _P]),
     ("dlm_refine_local", _I, [_P, _I, _I, _I, _P, _P, _P, _I, _P, _P, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
                               ctypes.POINTER(DlmStats), ctypes.POINTER(_I)]),
+    ("dlm_draft_workspace_bytes", _SZ, [_CFG, _I, _I, _I, _I]),
+    ("dlm_draft", _I, [_P, _I, _I, _I, _P, _P, _I, _I, _F, _P, _SZ, _P, ctypes.POINTER(DlmStats),
+                       ctypes.POINTER(_I)]),
+    ("dlm_draft_step", _I, [_P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _SZ, _P, _P, _P, _P, _P]),
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
     ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),

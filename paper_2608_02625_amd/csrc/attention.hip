@@ -5,6 +5,12 @@
 // so there is no causal or block mask.  Keys beyond S (tile padding) are the
 // only masked entries.
 //
+// The same kernel serves block-AR drafting (Sec. 3.3): there the queries are
+// the Sq rows of one window (the prompt, or one block) and the keys are the
+// first n_keys rows of a longer per-layer K/V cache of Skv rows (everything up
+// to the window's end).  Every window query sees exactly those keys, which is
+// the block-causal mask for a window that is one block or the prompt.
+//
 // One workgroup = 4 waves = 128 queries of one (batch, head); each wave owns 32
 // queries.  Per 64-key tile, K [64 keys][hd] and V^T [hd][64 keys] are copied
 // global -> LDS by buffer loads (two stages, XOR-swizzled 16-byte chunks).
@@ -49,8 +55,8 @@ __device__ __forceinline__ int chunk_key(int row) {
 
 template <int HD>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
-                                                   const bf16_t* Vt, bf16_t* __restrict__ O, int S,
-                                                   int H, int KV, float scale_log2, uint32_t k_bytes,
+                                                   const bf16_t* Vt, bf16_t* __restrict__ O, int Sq, int Skv,
+                                                   int n_keys, int H, int KV, float scale_log2, uint32_t k_bytes,
                                                    uint32_t v_bytes) {
     using C = AttnCfg<HD>;
     __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
@@ -60,16 +66,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int kvh = h / (H / KV);
     const int q = qb * 128 + wave * 32 + j;
-    const int VS = vt_stride(S);
+    const int VS = vt_stride(Skv);
     const int wv = wave;
 
-    const bf16_t* Qh = Q + ((int64_t)b * H + h) * S * HD;
-    // The last K tile reads up to 63 rows past S: rows of the next head
-    // (masked), or past the last head into the buffer's one-tile tail.  V^T
-    // rows are padded to whole tiles, so V^T reads stay inside their row.
+    const bf16_t* Qh = Q + ((int64_t)b * H + h) * Sq * HD;
+    // The last K tile reads up to 63 rows past n_keys: later rows of the same
+    // head, rows of the next head (all masked), or past the last head into the
+    // buffer's one-tile tail.  V^T rows are padded to whole tiles, so V^T
+    // reads stay inside their row.
     const buf_rsrc_t k_rsrc = make_rsrc(K, (int)k_bytes);
     const buf_rsrc_t v_rsrc = make_rsrc(Vt, (int)v_bytes);
-    const uint32_t k_base = (uint32_t)(((int64_t)b * KV + kvh) * S * HD * 2);
+    const uint32_t k_base = (uint32_t)(((int64_t)b * KV + kvh) * Skv * HD * 2);
     const uint32_t v_base = (uint32_t)(((int64_t)b * KV + kvh) * HD * VS * 2);
 
     // Per-lane byte offsets of this wave's copies (tile-relative; the key
@@ -108,7 +115,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 
     bf16x8 qf[C::NKS];
     {
-        const bf16_t* qp = Qh + (int64_t)min(q, S - 1) * HD + g * 8;
+        const bf16_t* qp = Qh + (int64_t)min(q, Sq - 1) * HD + g * 8;
 #pragma unroll
         for (int ks = 0; ks < C::NKS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qp + ks * 16);
     }
@@ -127,7 +134,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int vfrag = C::K_BYTES + j * C::V_ROW;
     const int vkey = chunk_key<C::V_CPR>(j);
 
-    const int nkt = (S + C::KEYS - 1) / C::KEYS;
+    const int nkt = (n_keys + C::KEYS - 1) / C::KEYS;
     issue(0, 0);
     for (int kt = 0; kt < nkt; ++kt) {
         wait_all_memory();                          // this wave's copies of tile kt landed
@@ -150,12 +157,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
                 st[c] = mfma32x32x16(kf, qf[ks], st[c]);
             }
         }
-        if (k0 + C::KEYS > S) {                     // last tile: keys past S do not exist
+        if (k0 + C::KEYS > n_keys) {                // last tile: keys past n_keys are not visible
 #pragma unroll
             for (int c = 0; c < 2; ++c)
 #pragma unroll
                 for (int e = 0; e < 16; ++e)
-                    if (k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= S) st[c][e] = -INFINITY;
+                    if (k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= n_keys) st[c][e] = -INFINITY;
         }
         float mt = -INFINITY;
 #pragma unroll
@@ -206,9 +213,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     }
 
     l_run += __shfl_xor(l_run, 32, 64);
-    if (q < S) {
+    if (q < Sq) {
         const float inv = 1.f / l_run;
-        bf16_t* orow = O + ((int64_t)b * S + q) * ((int64_t)H * HD) + (int64_t)h * HD;
+        bf16_t* orow = O + ((int64_t)b * Sq + q) * ((int64_t)H * HD) + (int64_t)h * HD;
 #pragma unroll
         for (int n = 0; n < C::NB; ++n)
 #pragma unroll
@@ -224,18 +231,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 }  // namespace
 
 hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, bf16_t* o, int B,
-                            int S, int H, int KV, int hd, hipStream_t st) {
-    const dim3 grid((S + 127) / 128, H, B);
+                            int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st) {
+    if (Sq <= 0 || n_keys <= 0 || n_keys > Skv) return hipErrorInvalidValue;
+    const dim3 grid((Sq + 127) / 128, H, B);
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     // byte sizes of the K buffer (with its one-tile tail) and of V^T
-    const int64_t kb = ((int64_t)B * KV * S + 64) * hd * 2, vb = (int64_t)B * KV * hd * vt_stride(S) * 2;
+    const int64_t kb = ((int64_t)B * KV * Skv + 64) * hd * 2, vb = (int64_t)B * KV * hd * vt_stride(Skv) * 2;
     if (kb >= 0x7fffffff || vb >= 0x7fffffff) return hipErrorInvalidValue;   // 32-bit buffer offsets
     if (hd == 128)
-        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, S, H, KV, scale_log2,
-                           (uint32_t)kb, (uint32_t)vb);
+        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, H, KV,
+                           scale_log2, (uint32_t)kb, (uint32_t)vb);
     else if (hd == 64)
-        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, S, H, KV, scale_log2,
-                           (uint32_t)kb, (uint32_t)vb);
+        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, H, KV,
+                           scale_log2, (uint32_t)kb, (uint32_t)vb);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

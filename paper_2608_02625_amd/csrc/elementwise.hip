@@ -177,6 +177,81 @@ __global__ void count_masks_kernel(const int32_t* __restrict__ tokens, int S, in
     if ((threadIdx.x & 63) == 0 && bm) atomicAdd(counter, (int)__popcll(bm));
 }
 
+// Block-AR drafting: tokens [B][S] = prompt ‖ all [MASK].
+__global__ void draft_init_kernel(const int32_t* __restrict__ prompt, int32_t* __restrict__ tokens, int P, int S,
+                                  int mask_id, int n) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n) return;
+    const int b = idx / S, s = idx - b * S;
+    tokens[idx] = s < P ? prompt[(int64_t)b * P + s] : mask_id;
+}
+
+// out [B][L] = tokens[b][c0 .. c0 + L) of a [B][S] sequence.
+__global__ void window_gather_kernel(const int32_t* __restrict__ tokens, int32_t* __restrict__ out, int S, int c0,
+                                     int L, int n) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n) return;
+    const int b = idx / L, i = idx - b * L;
+    out[idx] = tokens[(int64_t)b * S + c0 + i];
+}
+
+// One drafting step's unmasking on the L slots of a block, one workgroup per
+// sequence: quota = ceil(masked / steps_left); every masked slot with conf >=
+// tau is taken, or, when those are fewer than the quota, the quota masked
+// slots of highest confidence (equal confidences: lower position first).  A
+// slot's rank among the masked slots is counted directly (L <= 1024).
+// counters[0] += slots that took a real token, counters[2] += masked slots
+// left afterwards, counters[3] = 1 (one step; the dlm_stats layout).
+__global__ __launch_bounds__(256) void draft_select_kernel(int32_t* __restrict__ tokens, int S, int c0, int L,
+                                                           const int32_t* __restrict__ top1,
+                                                           const float* __restrict__ conf, float tau,
+                                                           int steps_left, int mask_id,
+                                                           int32_t* __restrict__ counters,
+                                                           int32_t* __restrict__ out_top1,
+                                                           float* __restrict__ out_conf) {
+    __shared__ float cs[1024];
+    __shared__ int ms[1024];
+    __shared__ int n_mask, n_above, n_unm, n_left;
+    const int b = blockIdx.x;
+    int32_t* row = tokens + (int64_t)b * S + c0;
+    if (threadIdx.x == 0) n_mask = n_above = n_unm = n_left = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < L; i += blockDim.x) {
+        const float c = conf[(int64_t)b * L + i];
+        const int m = row[i] == mask_id;
+        cs[i] = c;
+        ms[i] = m;
+        if (m) {
+            atomicAdd(&n_mask, 1);
+            if (c >= tau) atomicAdd(&n_above, 1);
+        }
+        if (out_top1) out_top1[(int64_t)b * L + i] = top1[(int64_t)b * L + i];
+        if (out_conf) out_conf[(int64_t)b * L + i] = c;
+    }
+    __syncthreads();
+    const int quota = (n_mask + steps_left - 1) / steps_left;
+    const int n_sel = max(quota, n_above);
+    for (int i = threadIdx.x; i < L; i += blockDim.x) {
+        if (!ms[i]) continue;
+        const float c = cs[i];
+        int rank = 0;
+        for (int j = 0; j < L; ++j) rank += ms[j] && (cs[j] > c || (cs[j] == c && j < i));
+        int t = mask_id;
+        if (rank < n_sel) {
+            t = top1[(int64_t)b * L + i];
+            row[i] = t;
+        }
+        if (t != mask_id) atomicAdd(&n_unm, 1);
+        else atomicAdd(&n_left, 1);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (n_unm) atomicAdd(&counters[0], n_unm);
+        if (n_left) atomicAdd(&counters[2], n_left);
+        if (b == 0) counters[3] = 1;
+    }
+}
+
 __global__ void zero_i32_kernel(int32_t* __restrict__ p, int n) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = 0;
@@ -256,6 +331,25 @@ void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int m
     const int n = B * D;
     hipLaunchKernelGGL(count_masks_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, S, P, D,
                        mask_id, counter, n);
+}
+
+void launch_draft_init(const int32_t* prompt, int32_t* tokens, int B, int P, int S, int mask_id, hipStream_t st) {
+    const int n = B * S;
+    hipLaunchKernelGGL(draft_init_kernel, dim3((n + 255) / 256), dim3(256), 0, st, prompt, tokens, P, S, mask_id, n);
+}
+
+void launch_window_gather(const int32_t* tokens, int32_t* out, int B, int S, int c0, int L, hipStream_t st) {
+    const int n = B * L;
+    hipLaunchKernelGGL(window_gather_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tokens, out, S, c0, L, n);
+}
+
+hipError_t launch_draft_select(int32_t* tokens, int B, int S, int c0, int L, const int32_t* top1, const float* conf,
+                               float tau, int steps_left, int mask_id, int32_t* counters, int32_t* out_top1,
+                               float* out_conf, hipStream_t st) {
+    if (L < 1 || L > 1024 || steps_left < 1 || c0 < 0 || c0 + L > S) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(draft_select_kernel, dim3(B), dim3(256), 0, st, tokens, S, c0, L, top1, conf, tau, steps_left,
+                       mask_id, counters, out_top1, out_conf);
+    return hipGetLastError();
 }
 
 void launch_zero_i32(int32_t* p, int n, hipStream_t st) {

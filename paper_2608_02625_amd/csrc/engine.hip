@@ -8,6 +8,9 @@
 //                 expert GEMMs/combine)]
 //         -> final rmsnorm of draft rows -> LM-head GEMM with fused softmax
 //            partials -> merge -> threshold edit.
+// Block-AR drafting runs the same layer sequence over one window of rows at a
+// time (the prompt, or one block), with K and V kept per layer in a cache that
+// spans the whole sequence.
 #include <math.h>
 #include <string.h>
 
@@ -253,6 +256,15 @@ struct Ctx {
     int B, P, D, S, T, R;
     bool h_ready = false;           // h already holds the next block's normalised input
     int pos_shift = 0;              // draft positions are P + shift + i (a span refined on its own)
+    // Drafting windows: the S rows of each sequence are positions q0 .. q0+S-1
+    // of a sequence of kv_seq positions whose K / V^T live in the per-layer
+    // caches kc / vc (kv_seq = 0: refinement, K and V^T of the S rows only).
+    int q0 = 0, kv_seq = 0;
+    bf16_t* kc = nullptr;
+    bf16_t* vc = nullptr;
+    size_t kc_layer = 0, vc_layer = 0;  // elements per layer
+    const float2* rope_all = nullptr;   // RoPE table of all kv_seq positions
+    bool kv_only = false;               // stop after the last layer's K/V (cache commit)
     template <class Tp>
     Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
     const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
@@ -326,9 +338,10 @@ dlm_status run_layer(Ctx& x, int l) {
     float* xs = x.at<float>(x.w.x);
     bf16_t* h = x.at<bf16_t>(x.w.h);
     bf16_t* q = x.at<bf16_t>(x.w.q);
-    bf16_t* k = x.at<bf16_t>(x.w.k);
-    bf16_t* v = x.at<bf16_t>(x.w.v);
+    bf16_t* k = x.kc ? x.kc + (size_t)l * x.kc_layer : x.at<bf16_t>(x.w.k);
+    bf16_t* v = x.vc ? x.vc + (size_t)l * x.vc_layer : x.at<bf16_t>(x.w.v);
     bf16_t* attn = x.at<bf16_t>(x.w.attn);
+    const int kvS = x.kv_seq ? x.kv_seq : x.S;
 
     if (!x.h_ready) LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g1), h, x.T, d, c.norm_eps, x.st));
     x.h_ready = false;
@@ -339,8 +352,10 @@ dlm_status run_layer(Ctx& x, int l) {
         a.q = q;
         a.k = k;
         a.v = v;
-        a.rope = x.at<float2>(x.w.rope);
+        a.rope = x.rope_all ? x.rope_all : x.at<float2>(x.w.rope);
         a.seq = x.S;
+        a.kv_seq = kvS;
+        a.pos0 = x.q0;
         a.n_heads = H;
         a.n_kv = KV;
         a.head_dim = hd;
@@ -348,9 +363,10 @@ dlm_status run_layer(Ctx& x, int l) {
         a.variant = big_tiles >= 192 ? 11 : 0;          // ping-pong 8-wave 256x256 tiles
         TRY(gemm(x, "gemm_qkv", a, EPI_QKV, false, 256, a.variant != 0 ? 256 : 128, 0));
     }
+    if (x.kv_only && l + 1 == c.n_layers) return DLM_OK;    // the cache holds this window's K/V now
     {
         prof_begin(x, "attention");
-        hipError_t e = launch_attention(q, k, v, attn, x.B, x.S, H, KV, hd, x.st);
+        hipError_t e = launch_attention(q, k, v, attn, x.B, x.S, kvS, x.q0 + x.S, H, KV, hd, x.st);
         prof_end(x, "attention");
         if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("attention: ") + hipGetErrorString(e));
     }
@@ -495,6 +511,130 @@ dlm_status step_impl(Ctx& x, int32_t* tokens, const dlm_edit_rule& rule, int32_t
     if (eos_out) HIP_TRY(hipMemcpyAsync(eos_out, eos, 4, hipMemcpyDeviceToDevice, x.st));
     return DLM_OK;
 }
+
+// ------------------------------------------------------------ block-AR drafting
+// Workspace of drafting (B, P, D, block): window buffers for max(P, block)
+// rows per sequence, then the per-layer K / V^T caches over all P + D
+// positions, the RoPE table of those positions, the window's tokens and the
+// token state [B][P + D].
+struct DraftPlan {
+    Workspace w;
+    size_t kc = 0, vc = 0, rope = 0, wtok = 0, tokens = 0, total = 0;
+    size_t kc_layer = 0, vc_layer = 0;
+    int rows = 0;
+};
+
+DraftPlan plan_draft(const dlm_config& c, int B, int P, int D, int blk) {
+    DraftPlan p;
+    p.rows = std::max(P, std::min(blk, D));
+    p.w = plan_workspace(c, B, 0, p.rows);
+    size_t total = p.w.total;
+    auto add = [&](int64_t bytes) {
+        const size_t off = total;
+        total = align_up(total + (size_t)std::max<int64_t>(bytes, 1));
+        return off;
+    };
+    const int64_t S = (int64_t)P + D;
+    const int hd = c.head_dim;
+    p.kc_layer = (size_t)B * c.n_kv_heads * S * hd;
+    p.vc_layer = (size_t)B * c.n_kv_heads * hd * vt_stride((int)S);
+    p.kc = add(((int64_t)c.n_layers * p.kc_layer + 64 * hd) * 2);     // + one 64-key tile of tail
+    p.vc = add((int64_t)c.n_layers * p.vc_layer * 2);
+    p.rope = add(S * (hd / 2) * 8);
+    p.wtok = add((int64_t)B * p.rows * 4);
+    p.tokens = add((int64_t)B * S * 4);
+    p.total = total;
+    return p;
+}
+
+std::string check_draft_shape(int B, int P, int D, int blk) {
+    std::string e = check_shape(B, P, D);
+    if (!e.empty()) return e;
+    if (blk < 1 || blk > 1024) return "block_len must be in [1, 1024]";
+    return "";
+}
+
+dlm_status check_draft(dlm_model* m, int B, int P, int D, int blk, void* ws, size_t ws_bytes, DraftPlan* p) {
+    if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+    const std::string e = check_draft_shape(B, P, D, blk);
+    if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
+    *p = plan_draft(m->cfg, B, P, D, blk);
+    if (!ws) return fail(DLM_ERR_INVALID_ARG, "workspace is NULL");
+    if (ws_bytes < p->total)
+        return fail(DLM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(p->total) + " bytes, got " +
+                                           std::to_string(ws_bytes));
+    if (((uintptr_t)ws) % kAlign) return fail(DLM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    return DLM_OK;
+}
+
+struct Drafter {
+    dlm_model* m;
+    char* ws;
+    const DraftPlan& p;
+    hipStream_t st;
+    int B, P, D, S, blk;
+
+    // Context of the window of L rows starting at position c0 of every sequence.
+    Ctx window(int c0, int L) const {
+        Ctx x{m, m->cfg, ws, p.w, st, B, 0, L, L, B * L, B * L};
+        x.q0 = c0;
+        x.kv_seq = S;
+        x.kc = x.at<bf16_t>(p.kc);
+        x.vc = x.at<bf16_t>(p.vc);
+        x.kc_layer = p.kc_layer;
+        x.vc_layer = p.vc_layer;
+        x.rope_all = x.at<float2>(p.rope);
+        return x;
+    }
+    int32_t* counters() const { return reinterpret_cast<int32_t*>(ws + p.w.counters); }
+
+    // Forward of one window of the token state: all layers' K/V of its rows go
+    // into the caches; with head, also the top-1 / confidence of its rows.
+    dlm_status run(const int32_t* tokens, int c0, int L, bool head) const {
+        Ctx x = window(c0, L);
+        const dlm_config& c = m->cfg;
+        x.kv_only = !head;
+        int32_t* wtok = x.at<int32_t>(p.wtok);
+        LAUNCH(x, "window_gather", launch_window_gather(tokens, wtok, B, S, c0, L, st));
+        LAUNCH(x, "embed", launch_embed(wtok, x.wt(m->plan.emb), x.at<float>(p.w.x), x.T, c.d_model, c.vocab, st));
+        for (int l = 0; l < c.n_layers; ++l) TRY(run_layer(x, l));
+        if (head) TRY(run_head(x, x.at<int32_t>(p.w.top1), x.at<float>(p.w.conf), x.at<float>(p.w.maxlogit), nullptr));
+        HIP_TRY(hipGetLastError());
+        return DLM_OK;
+    }
+
+    // Fresh caches (zero, so the attention's tile reads past the visible keys
+    // meet finite values), the RoPE table, and the prompt's K/V: the prompt
+    // attends to itself only.
+    dlm_status begin(const int32_t* tokens) const {
+        const dlm_config& c = m->cfg;
+        Ctx x = window(0, 1);
+        launch_fill_bf16(x.kc, (uint64_t)c.n_layers * p.kc_layer + 64 * c.head_dim, 0, st);
+        launch_fill_bf16(x.vc, (uint64_t)c.n_layers * p.vc_layer, 0, st);
+        launch_rope_table(x.at<float2>(p.rope), S, c.head_dim / 2, (double)c.rope_theta, S, 0, st);
+        HIP_TRY(hipGetLastError());
+        if (P > 0) TRY(run(tokens, 0, P, false));
+        return DLM_OK;
+    }
+
+    int block_start(int k) const { return P + k * blk; }
+    int block_rows(int k) const { return std::min(blk, S - block_start(k)); }
+
+    // One denoising step on block k: forward of the block's window, then the
+    // unmasking.  counters: [0] unmasked, [2] masked left in the block, [3] = 1.
+    dlm_status step(int32_t* tokens, int k, float tau, int steps_left, int32_t* top1_out, float* conf_out) const {
+        const int c0 = block_start(k), L = block_rows(k);
+        TRY(run(tokens, c0, L, true));
+        Ctx x = window(c0, L);
+        launch_zero_i32(counters(), 4, st);
+        prof_begin(x, "draft_select");
+        hipError_t e = launch_draft_select(tokens, B, S, c0, L, x.at<int32_t>(p.w.top1), x.at<float>(p.w.conf), tau,
+                                           steps_left, m->cfg.mask_id, counters(), top1_out, conf_out, st);
+        prof_end(x, "draft_select");
+        if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("draft_select: ") + hipGetErrorString(e));
+        return DLM_OK;
+    }
+};
 
 dlm_status check_rule(const dlm_config& c, const dlm_edit_rule* rule) {
     if (!rule) return fail(DLM_ERR_INVALID_ARG, "rule is NULL");
@@ -707,6 +847,79 @@ dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t d
     const dlm_edit_rule rule{threshold, threshold, -1};
     return dlm_refine_ex(m, batch, prompt_len, draft_len, d_prompt, d_draft, d_mask, n_steps, &rule, d_workspace,
                          workspace_bytes, hip_stream, h_stats, nullptr);
+}
+
+size_t dlm_draft_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                                 int32_t block_len) {
+    if (!validate(cfg).empty() || !check_draft_shape(batch, prompt_len, draft_len, block_len).empty()) return 0;
+    return plan_draft(*cfg, batch, prompt_len, draft_len, block_len).total;
+}
+
+dlm_status dlm_draft_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, int32_t block_len,
+                          int32_t block_index, int32_t steps_left, float threshold, int32_t* d_tokens,
+                          void* d_workspace, size_t workspace_bytes, void* hip_stream, int32_t* d_top1,
+                          float* d_conf, float* d_max_logit, dlm_stats* d_stats) {
+    DraftPlan p;
+    TRY(check_draft(m, batch, prompt_len, draft_len, block_len, d_workspace, workspace_bytes, &p));
+    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+    const int n_blocks = (draft_len + block_len - 1) / block_len;
+    if (block_index < 0 || block_index >= n_blocks) return fail(DLM_ERR_INVALID_ARG, "block_index out of range");
+    if (steps_left < 1) return fail(DLM_ERR_INVALID_ARG, "steps_left < 1");
+    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len,
+                     prompt_len + draft_len, block_len};
+    TRY(dr.begin(d_tokens));
+    for (int j = 0; j < block_index; ++j) TRY(dr.run(d_tokens, dr.block_start(j), block_len, false));
+    TRY(dr.step(d_tokens, block_index, threshold, steps_left, d_top1, d_conf));
+    if (d_stats) HIP_TRY(hipMemcpyAsync(d_stats, dr.counters(), sizeof(dlm_stats), hipMemcpyDeviceToDevice, dr.st));
+    if (d_max_logit)
+        HIP_TRY(hipMemcpyAsync(d_max_logit, dr.ws + p.w.maxlogit, (size_t)batch * dr.block_rows(block_index) * 4,
+                               hipMemcpyDeviceToDevice, dr.st));
+    return DLM_OK;
+}
+
+dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, const int32_t* d_prompt,
+                     int32_t* d_draft, int32_t block_len, int32_t steps_per_block, float threshold,
+                     void* d_workspace, size_t workspace_bytes, void* hip_stream, dlm_stats* h_stats,
+                     int32_t* h_block_steps) {
+    DraftPlan p;
+    TRY(check_draft(m, batch, prompt_len, draft_len, block_len, d_workspace, workspace_bytes, &p));
+    if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
+    if (steps_per_block < 1) return fail(DLM_ERR_INVALID_ARG, "steps_per_block < 1");
+    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    const int S = prompt_len + draft_len;
+    const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len, S, block_len};
+    int32_t* tokens = reinterpret_cast<int32_t*>((char*)d_workspace + p.tokens);
+    launch_draft_init(d_prompt, tokens, batch, prompt_len, S, m->cfg.mask_id, dr.st);
+    HIP_TRY(hipGetLastError());
+    TRY(dr.begin(tokens));
+    const int n_blocks = (draft_len + block_len - 1) / block_len;
+    dlm_stats tot{0, 0, 0, 0};
+    for (int k = 0; k < n_blocks; ++k) {
+        int used = 0;
+        for (int t = 0; t < steps_per_block; ++t) {
+            TRY(dr.step(tokens, k, threshold, steps_per_block - t, nullptr, nullptr));
+            int32_t c[4] = {};
+            HIP_TRY(hipMemcpyAsync(c, dr.counters(), sizeof(c), hipMemcpyDeviceToHost, dr.st));
+            HIP_TRY(hipStreamSynchronize(dr.st));
+            ++used;
+            tot.n_unmasked += c[0];
+            if (c[2] == 0) break;                     // no [MASK] left in the block
+        }
+        tot.steps_run += used;
+        if (h_block_steps) h_block_steps[k] = used;
+        if (k + 1 < n_blocks) TRY(dr.run(tokens, dr.block_start(k), dr.block_rows(k), false));   // commit its K/V
+    }
+    launch_copy_draft_out(tokens, d_draft, batch, S, prompt_len, draft_len, dr.st);
+    launch_zero_i32(dr.counters(), 4, dr.st);
+    launch_count_masks(tokens, batch, S, prompt_len, draft_len, m->cfg.mask_id, dr.counters() + 2, dr.st);
+    HIP_TRY(hipGetLastError());
+    dlm_stats fin{};
+    HIP_TRY(hipMemcpyAsync(&fin, dr.counters(), sizeof(fin), hipMemcpyDeviceToHost, dr.st));
+    HIP_TRY(hipStreamSynchronize(dr.st));
+    tot.n_masked_left = fin.n_masked_left;
+    if (h_stats) *h_stats = tot;
+    return DLM_OK;
 }
 
 dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,

@@ -80,7 +80,7 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
                                              int lrow0, int lcol0) {
     constexpr int HALF = HD / 2, SPH = HD / 32, POFF = HD / 64;
     const int Hq = a.n_heads * HD, Hk = a.n_kv * HD;
-    const int S = a.seq;
+    const int S = a.seq, SK = a.kv_seq;
     // A wave's 128 rows start on a head boundary, and the Q/K/V boundaries are
     // head boundaries: the wave is wholly inside Q, K or V (or past M).
     const int wrow = m0 + (lrow0 & ~127);
@@ -91,6 +91,7 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
         const int t = n0 + lcol0 + j * 32;                    // token
         if (t >= a.N) continue;
         const int b = t / S, s = t - b * S;
+        const int sk = s + a.pos0;                            // position in K / V^T and the RoPE table
         if (rotate) {
             // (cos, sin) of the lane's 4 consecutive pairs for each first-half
             // 32-row block and each group q, all loaded before use.
@@ -100,7 +101,7 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int r0 = (lrow0 & 127) + ih * 32 + 8 * q;       // row within the head pair block
-                    const float4* p = reinterpret_cast<const float4*>(a.rope + s * HALF + (r0 % HALF));
+                    const float4* p = reinterpret_cast<const float4*>(a.rope + sk * HALF + (r0 % HALF));
                     cs[ih][q][0] = p[0];
                     cs[ih][q][1] = p[1];
                 }
@@ -125,18 +126,18 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
                             v[r] = acc[i][j][4 * q + r] * cz[r] + acc[(i + TM - POFF) % TM][j][4 * q + r] * sn[r];
                     }
                     bf16_t* dst = f0 < Hq ? a.q + (((int64_t)b * a.n_heads + f0 / HD) * S + s) * HD + hi0
-                                          : a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * S + s) * HD + hi0;
+                                          : a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * SK + sk) * HD + hi0;
                     *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
                 }
         } else {
             // V^T: per accumulator 4 rows (features) of one key column
-            const int vs = vt_stride(S);
+            const int vs = vt_stride(SK);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int fv = m0 + lrow0 + i * 32 + 8 * q - Hq - Hk;
-                    bf16_t* col = a.v + ((int64_t)(b * a.n_kv + fv / HD) * HD + fv % HD) * vs + vt_pos(s);
+                    bf16_t* col = a.v + ((int64_t)(b * a.n_kv + fv / HD) * HD + fv % HD) * vs + vt_pos(sk);
 #pragma unroll
                     for (int r = 0; r < 4; ++r) col[(int64_t)r * vs] = f32_to_bf16(acc[i][j][4 * q + r]);
                 }

@@ -27,7 +27,7 @@ enum GemmEpilogue {
     EPI_F32 = 1,      // out_f32[row][col]
     EPI_RESID = 2,    // resid_f32[row][col] += acc
     EPI_SWIGLU = 3,   // out_bf16[row][f] = silu(gate) * up, gate/up interleaved in 32-col blocks
-    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K [B][KV][S][hd], V^T (vt_pos)
+    EPI_QKV = 4,      // RoPE on q,k; scatter to Q [B][H][S][hd], K [B][KV][Skv][hd], V^T (vt_pos)
     EPI_LMHEAD = 5,   // rows = vocab, cols = tokens: per-(vocab tile, token) softmax partials
     EPI_F32_T = 6,    // out_f32[col][row] (transposed store)
 };
@@ -54,8 +54,12 @@ struct GemmArgs {
     bf16_t* q;
     bf16_t* k;
     bf16_t* v;
-    const float2* rope;       // [S][hd/2] (cos, sin)
+    const float2* rope;       // [kv_seq][hd/2] (cos, sin), by absolute position
     int seq, n_heads, n_kv, head_dim;
+    // K and V^T hold kv_seq rows per sequence; token s of a sequence (s < seq)
+    // sits at position pos0 + s there and in the RoPE table (refinement: kv_seq
+    // = seq, pos0 = 0).  Q keeps seq rows per sequence.
+    int kv_seq, pos0;
     // EPI_LMHEAD: partials [2 * ceil(M/BM) half tiles][N] (m, idx, s) stored as float4
     float4* partials;
 };
@@ -67,8 +71,10 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, bool grouped, int bm, int bn,
 
 // ----------------------------------------------------------------- attention.hip
 // Non-causal attention over Q [B][H][S][hd], K, V [B][KV][S][hd]; O [B*S][H*hd] bf16.
+// Draft windows: Q holds Sq rows per sequence, K and V^T hold Skv rows per
+// sequence of which the first n_keys are visible (n_keys <= Skv); O [B*Sq][H*hd].
 hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* v, bf16_t* o, int B,
-                            int S, int H, int KV, int hd, hipStream_t st);
+                            int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st);
 
 // ----------------------------------------------------------------- elementwise.hip
 void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
@@ -99,6 +105,15 @@ void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, 
 void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int mask_id,
                         int32_t* counter, hipStream_t st);
 void launch_zero_i32(int32_t* p, int n, hipStream_t st);
+// Block-AR drafting: tokens [B][S] = prompt ‖ [MASK] ...; out [B][L] =
+// tokens[:, c0 : c0 + L]; the unmasking of one step on the block at c0 of
+// length L <= 1024 (top1 / conf [B][L]; counters[0] += slots given a real
+// token, counters[2] += masked slots left, counters[3] = 1).
+void launch_draft_init(const int32_t* prompt, int32_t* tokens, int B, int P, int S, int mask_id, hipStream_t st);
+void launch_window_gather(const int32_t* tokens, int32_t* out, int B, int S, int c0, int L, hipStream_t st);
+hipError_t launch_draft_select(int32_t* tokens, int B, int S, int c0, int L, const int32_t* top1, const float* conf,
+                               float tau, int steps_left, int mask_id, int32_t* counters, int32_t* out_top1,
+                               float* out_conf, hipStream_t st);
 // Zero the V^T positions of keys S .. S64-1 in every one of `rows` rows.
 void launch_vt_pad_zero(bf16_t* vt, int64_t rows, int S, hipStream_t st);
 

@@ -182,6 +182,49 @@ class Refiner:
         return draft, out
 
     # -------------------------------------------------------------- test hooks
+    # ------------------------------------------------------- block-AR drafting
+    def draft_workspace(self, batch: int, prompt_len: int, draft_len: int, block_len: int) -> torch.Tensor:
+        key = ("draft", batch, prompt_len, draft_len, block_len)
+        ws = self._ws.get(key)
+        if ws is None:
+            n = self.lib.dlm_draft_workspace_bytes(ctypes.byref(self.cfg), batch, prompt_len, draft_len, block_len)
+            if n == 0:
+                raise ValueError(f"invalid drafting shape {key[1:]}")
+            ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+            self._ws[key] = ws
+        return ws
+
+    def draft(self, prompt: torch.Tensor, draft_len: int, block_len: int, steps_per_block: int,
+              threshold: float):
+        """Block-AR draft of draft_len tokens after prompt [B, P] (int32, on the
+        device).  Returns (draft [B, draft_len] int32, stats dict with
+        block_steps)."""
+        B, P = prompt.shape
+        ws = self.draft_workspace(B, P, draft_len, block_len)
+        out = torch.empty(B, draft_len, dtype=torch.int32, device=self.device)
+        st = DlmStats()
+        n_blocks = -(-draft_len // block_len)
+        steps = (ctypes.c_int32 * n_blocks)()
+        check(self.lib.dlm_draft(self._handle, B, P, draft_len, _ptr(prompt) if P else None, out.data_ptr(),
+                                 block_len, steps_per_block, float(threshold), ws.data_ptr(), ws.numel(),
+                                 self.stream, ctypes.byref(st), steps), "dlm_draft")
+        d = st.as_dict()
+        d["block_steps"] = list(steps)
+        return out, d
+
+    def draft_step(self, tokens: torch.Tensor, prompt_len: int, block_len: int, block_index: int,
+                   steps_left: int, threshold: float, top1: torch.Tensor | None = None,
+                   conf: torch.Tensor | None = None, stats: torch.Tensor | None = None,
+                   max_logit: torch.Tensor | None = None):
+        """One drafting step on block block_index of tokens [B, P + D] (in place)."""
+        B, S = tokens.shape
+        D = S - prompt_len
+        ws = self.draft_workspace(B, prompt_len, D, block_len)
+        check(self.lib.dlm_draft_step(self._handle, B, prompt_len, D, block_len, block_index, steps_left,
+                                      float(threshold), tokens.data_ptr(), ws.data_ptr(), ws.numel(), self.stream,
+                                      _ptr(top1), _ptr(conf), _ptr(max_logit), _ptr(stats)), "dlm_draft_step")
+        return tokens
+
     def debug_forward(self, tokens: torch.Tensor, prompt_len: int, want_logits: bool = False):
         B, S = tokens.shape
         D = S - prompt_len

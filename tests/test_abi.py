@@ -64,6 +64,14 @@ def test_size_queries_and_validation():
     assert ws > 5120 * 2048 * 4
     assert lib.dlm_workspace_bytes(ctypes.byref(cfg), 0, 256, 384) == 0
     assert lib.dlm_workspace_bytes(ctypes.byref(cfg), 8, 256, 0) == 0
+    # drafting: the per-layer K and V^T caches of all 640 positions come on top
+    # of the window buffers (20 layers x 8 x 4 kv heads x 640 x 128 x 2 bytes each)
+    cfg_kv = dict(zip([f for f, _ in L.DlmConfig._fields_], [getattr(cfg, f) for f, _ in L.DlmConfig._fields_]))
+    dw = lib.dlm_draft_workspace_bytes(ctypes.byref(cfg), 8, 256, 384, 64)
+    cache = 2 * cfg_kv["n_layers"] * 8 * cfg_kv["n_kv_heads"] * 640 * cfg_kv["head_dim"] * 2
+    assert dw >= cache + lib.dlm_workspace_bytes(ctypes.byref(cfg), 8, 0, 256)
+    assert lib.dlm_draft_workspace_bytes(ctypes.byref(cfg), 8, 256, 384, 0) == 0
+    assert lib.dlm_draft_workspace_bytes(ctypes.byref(cfg), 8, 256, 384, 1025) == 0
     for bad in (dict(head_dim=96), dict(top_k=9), dict(mask_id=157184), dict(n_heads=15),
                 dict(expert_ffn_dim=100), dict(n_experts=300), dict(vocab=1)):
         assert lib.dlm_weights_bytes(ctypes.byref(_cfg(L, **bad))) == 0, bad
@@ -83,5 +91,7 @@ def test_errors_are_reported_without_gpu_work():
     assert st == -5 and b"too small" in lib.dlm_last_error()
     assert lib.dlm_refine_step(None, 1, 1, 1, None, 0.5, None, 0, None, None, None, None) == -1
     assert lib.dlm_refine(None, 1, 1, 1, None, None, None, 1, 0.5, None, 0, None, None) == -1
+    assert lib.dlm_draft(None, 1, 1, 64, None, None, 64, 16, 0.25, None, 0, None, None, None) == -1
+    assert lib.dlm_draft_step(None, 1, 1, 64, 64, 0, 16, 0.25, None, None, 0, None, None, None, None, None) == -1
     with pytest.raises(L.DlmError):
         L.check(-1, "x")
