@@ -168,6 +168,125 @@ def bench_local(args, w, R, tokens0):
     }), flush=True)
 
 
+def cpu_baseline_draft(w, block, steps_avg):
+    """Oracle time of one drafting step on block 0 of batch row 0 (prompt +
+    one block under the block mask): one layer timed, extrapolated to all
+    layers, plus the LM-head reduction of the block's rows; scaled to drafted
+    positions per second with the GPU run's average steps per block."""
+    import numpy as np
+    import oracle
+    from oracle.refine import layer_forward, lm_head_reduce
+    from workloads import make_inputs
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    shape = w.model
+    W = oracle.OracleWeights(shape, w.weight_seed, cache_layers=False)
+    prompt, _, _ = make_inputs(w, batch=1)
+    P = w.prompt_len
+    tokens = np.concatenate([prompt, np.full((1, block), shape.mask_id, dtype=np.int32)], 1)
+    lim = oracle.block_key_limit(P, P + block, block)
+    x = W.embed_rows(tokens).astype(np.float64)
+    L0 = W.layer(0)
+    W.lm_head()
+    t0 = time.perf_counter()
+    x, _ = layer_forward(shape, L0, x, key_limit=lim)
+    t1 = time.perf_counter()
+    lm_head_reduce(W, x[0, P:])
+    t2 = time.perf_counter()
+    t_step = (t1 - t0) * shape.n_layers + (t2 - t1)
+    return {
+        "value": block / (steps_avg * t_step),
+        "unit": "drafted positions/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"one drafting step on block 0 of batch row 0 of {w.name} ({P} prompt + {block} block "
+                   f"tokens, block-causal): 1 of {shape.n_layers} layers timed ({t1 - t0:.2f} s), LM-head "
+                   f"reduction of {block} rows ({t2 - t1:.2f} s); {steps_avg:.2f} steps per block as on the "
+                   f"GPU; later blocks cost the oracle more (it recomputes the prefix); float64 NumPy"),
+    }
+
+
+def bench_draft(args, w, R, prompt_np):
+    """Block-AR drafting: a step is one whole draft of the batch (prefill of
+    the prompt, every block's denoising steps, the K/V commit of each finished
+    block).  The dominant kernel, the routed-expert gate/up GEMM of a block
+    window, streams every expert's weights once per launch: HBM-bound."""
+    import numpy as np
+    import torch
+    shape = w.model
+    B, P, D = w.batch, w.prompt_len, w.draft_len
+    b, s, tau = args.draft_block, args.draft_steps, args.draft_threshold
+    prompt = torch.tensor(prompt_np, device="cuda")
+    R.draft_workspace(B, P, D, b)
+    for _ in range(args.warmup):
+        R.draft(prompt, D, b, s, tau)
+    torch.cuda.synchronize()
+    print(f"[bench] draft warmup done; timing {args.steps} drafts", file=sys.stderr, flush=True)
+    kname = "gemm_expert_gate_up"
+    R.set_profiling(kname)
+    stats = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        _, st = R.draft(prompt, D, b, s, tau)
+        stats.append(st)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    launches = [ms for (n, ms) in R.profile_read() if n == kname]
+    R.set_profiling(None)
+    ms_draft = (t1 - t0) * 1e3 / args.steps
+    n_blocks = -(-D // b)
+    steps_run = stats[-1]["steps_run"]
+    L = shape.n_layers
+    # per draft: prefill (layers 0..L-2 reach the experts), steps x L, commits x (L-1)
+    per_call = (L - 1 if P else 0) + steps_run * L + (n_blocks - 1) * (L - 1)
+    assert len(launches) == per_call * args.steps, (len(launches), per_call)
+    win = []
+    for c in range(args.steps):
+        seg = launches[c * per_call:(c + 1) * per_call]
+        win.extend(seg[(L - 1 if P else 0):])                 # block windows only
+    k_avg_ms = float(np.mean(win))
+    T = B * b
+    G = shape.n_experts + shape.n_shared_experts
+    rows = T * shape.top_k + T * shape.n_shared_experts
+    F, d = shape.expert_ffn_dim, shape.d_model
+    k_bytes = G * 2 * F * d * 2 + rows * d * 2 + rows * F * 2    # every expert's weights, gathered rows, output
+    achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
+    passes = (1 if P else 0) + steps_run + n_blocks - 1
+    out = {
+        "metric": f"drafted positions/sec per block-AR draft (b{b}, s{s}, t{tau})",
+        "value": B * D / (ms_draft * 1e-3), "unit": "drafted positions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_draft, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name} draft", "batch": B, "prompt_len": P, "draft_len": D, "block_len": b,
+                   "steps_per_block": s, "threshold": tau},
+        "draft_stats": {"steps_run": steps_run, "block_steps": stats[-1]["block_steps"],
+                        "window_passes": passes, "ms_per_window_pass": ms_draft / passes},
+        "roofline": {"kernel": kname + " (block window)", "bound": "hbm", "achieved": achieved,
+                     "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": achieved / (PEAK_HBM / 1e9),
+                     "traffic": None, "launches": len(win), "avg_ms": k_avg_ms, "bytes_per_launch": k_bytes},
+    }
+    if args.kernel_table:
+        R.set_profiling("*")
+        R.draft(prompt, D, b, s, tau)
+        rows_ = R.profile_read()
+        R.set_profiling(None)
+        agg = {}
+        for n, ms in rows_:
+            a = agg.setdefault(n, [0, 0.0])
+            a[0] += 1
+            a[1] += ms
+        out["kernel_table_ms"] = {n: round(v[1], 4) for n, v in sorted(agg.items(), key=lambda kv: -kv[1][1])}
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline_draft(w, b, steps_run / n_blocks)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -179,6 +298,11 @@ def main():
     ap.add_argument("--kernel-table", action="store_true", help="also time every kernel (separate pass)")
     ap.add_argument("--local-span", type=int, default=0,
                     help="time local refinement instead: one pass over every draft chunk of this many tokens")
+    ap.add_argument("--draft", action="store_true",
+                    help="time block-AR drafting of the workload's draft length instead")
+    ap.add_argument("--draft-block", type=int, default=64)
+    ap.add_argument("--draft-steps", type=int, default=16)
+    ap.add_argument("--draft-threshold", type=float, default=0.25)
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (reference for memory counters)")
     args = ap.parse_args()
@@ -218,6 +342,9 @@ def main():
 
     if args.local_span:
         bench_local(args, w, R, tokens0)
+        return
+    if args.draft:
+        bench_draft(args, w, R, prompt.astype(np.int32))
         return
     for _ in range(args.warmup):
         R.refine_step(tokens, P, w.threshold)
