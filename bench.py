@@ -287,6 +287,78 @@ def bench_draft(args, w, R, prompt_np):
     print(json.dumps(out), flush=True)
 
 
+def bench_cascade(args, w, R, prompt_np):
+    """Two-model cascade: a step is one whole dlm_cascade of the batch (block-AR
+    draft with the drafter, then up to n refinement passes with the refiner).
+    `value` uses the model time the library reports (drafting + refinement,
+    the timing convention of Sec. 5.3 / App. A); the roofline row is the
+    refiner's gate/up expert GEMM."""
+    import dataclasses
+    import numpy as np
+    import torch
+    from paper_2608_02625_amd import Refiner, cascade
+    from workloads import MODELS
+    shape = w.model
+    B, P, D = w.batch, w.prompt_len, w.draft_len
+    b, s, tau = args.draft_block, args.draft_steps, args.draft_threshold
+    n_ref, t_ref = args.refine_steps, args.refine_threshold
+    dshape = MODELS[args.drafter]
+    print(f"[bench] drafter {args.drafter}: loading synthetic weights", file=sys.stderr, flush=True)
+    Rd = Refiner(dshape.as_dict(), w.weight_seed + 1)
+    prompt = torch.tensor(prompt_np, device="cuda")
+    for _ in range(args.warmup):
+        cascade(Rd, R, prompt, D, b, s, tau, n_ref, t_ref, t_ref)
+    torch.cuda.synchronize()
+    print(f"[bench] cascade warmup done; timing {args.steps} cascades", file=sys.stderr, flush=True)
+    kname = "gemm_expert_gate_up"
+    R.set_profiling(kname)
+    stats = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        stats.append(cascade(Rd, R, prompt, D, b, s, tau, n_ref, t_ref, t_ref)[1])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kt = [ms for (n, ms) in R.profile_read() if n == kname]
+    R.set_profiling(None)
+    ms_wall = (t1 - t0) * 1e3 / args.steps
+    ms_model = float(np.mean([st["draft_ms"] + st["refine_ms"] for st in stats]))
+    k_avg_ms = float(np.mean(kt))
+    k_flops = kernel_flops(kname, shape, B, P, D)
+    achieved = k_flops / (k_avg_ms * 1e-3) / 1e12
+    last = stats[-1]
+    out = {
+        "metric": f"cascade positions/sec, draft ({args.drafter}, b{b} s{s} t{tau}) + refine ({w.name}, "
+                  f"{D}x{n_ref}, t{t_ref}), model time",
+        "value": B * D / (ms_model * 1e-3), "unit": "generated positions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_wall, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name} cascade", "drafter": args.drafter, "batch": B, "prompt_len": P,
+                   "draft_len": D, "block_len": b, "steps_per_block": s, "draft_threshold": tau,
+                   "refine_steps": n_ref, "refine_threshold": t_ref},
+        "cascade": {"model_ms": ms_model, "draft_ms": float(np.mean([st["draft_ms"] for st in stats])),
+                    "refine_ms": float(np.mean([st["refine_ms"] for st in stats])),
+                    "draft_passes": last["draft_passes"], "refine_passes": last["refine_passes"],
+                    "passes": last["draft_passes"] + last["refine_passes"],
+                    "refine_stop_reason": last["refine_stop_reason"], "refine_stats": last["refine"]},
+        "roofline": {"kernel": kname + " (refiner)", "bound": "mfma", "achieved": achieved,
+                     "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": achieved / (PEAK_BF16 / 1e12),
+                     "traffic": None, "launches": len(kt), "avg_ms": k_avg_ms, "flops_per_launch": k_flops},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        wd = dataclasses.replace(w, model=dshape, weight_seed=w.weight_seed + 1)
+        cd = cpu_baseline_draft(wd, b, last["draft_passes"] / (-(-D // b)))
+        cr = cpu_baseline(w)
+        t_ex = D / cd["value"] + last["refine_passes"] * D / cr["value"]
+        out["cpu_baseline"] = {"value": D / t_ex, "unit": "generated positions/s", "cores": cr["cores"],
+                               "kind": "oracle",
+                               "sample": "drafter: " + cd["sample"] + " || refiner: " + cr["sample"] +
+                                         f" || combined as D / (D / draft rate + {last['refine_passes']} x D / "
+                                         f"refine rate) for one row"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -303,6 +375,11 @@ def main():
     ap.add_argument("--draft-block", type=int, default=64)
     ap.add_argument("--draft-steps", type=int, default=16)
     ap.add_argument("--draft-threshold", type=float, default=0.25)
+    ap.add_argument("--cascade", action="store_true",
+                    help="time the two-model cascade (drafter --drafter, refiner = the workload's model)")
+    ap.add_argument("--drafter", default="mini_drafter")
+    ap.add_argument("--refine-steps", type=int, default=4)
+    ap.add_argument("--refine-threshold", type=float, default=0.20)
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (reference for memory counters)")
     args = ap.parse_args()
@@ -345,6 +422,9 @@ def main():
         return
     if args.draft:
         bench_draft(args, w, R, prompt.astype(np.int32))
+        return
+    if args.cascade:
+        bench_cascade(args, w, R, prompt.astype(np.int32))
         return
     for _ in range(args.warmup):
         R.refine_step(tokens, P, w.threshold)

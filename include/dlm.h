@@ -271,6 +271,44 @@ dlm_status dlm_draft_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32
                           float* d_conf, float* d_max_logit, dlm_stats* d_stats);
 
 /*
+ * Speculative correction with two models (Sec. 4.3: a smaller drafter, the
+ * larger refiner; Sec. 4.2: the cost counted as K x T_d drafting passes plus
+ * T_r refinement passes; Sec. 5.3 / App. A: model time = drafting + refinement
+ * time only).
+ *
+ * dlm_cascade: dlm_draft with `drafter` (blocks of block_len, up to
+ *   steps_per_block steps, draft_threshold), then dlm_refine_ex with `refiner`
+ *   on the finished draft (no mask set; up to n_refine_steps passes under
+ *   *rule).  The two models must share vocab and mask_id.  d_prompt int32
+ *   [batch][prompt_len] (may be NULL when prompt_len is 0), d_draft int32
+ *   [batch][draft_len] receives the refined draft.  One workspace serves both
+ *   stages (they run one after the other): dlm_cascade_workspace_bytes, the
+ *   larger of the two stages' sizes.  h_stats (host, may be NULL): the draft
+ *   and refine stats, the pass counts of each stage, the refine stop reason
+ *   (as dlm_refine_ex) and the host wall-clock milliseconds of each stage
+ *   (each stage returns with its output written).  Synchronises the stream.
+ *   Errors as dlm_draft and dlm_refine_ex; models of different vocabularies
+ *   -> DLM_ERR_INVALID_ARG.
+ */
+typedef struct dlm_cascade_stats {
+    dlm_stats draft;           /* as dlm_draft's h_stats */
+    dlm_stats refine;          /* as dlm_refine_ex's h_stats */
+    int32_t draft_passes;      /* K x (steps used per block), summed over blocks */
+    int32_t refine_passes;     /* T_r actually run */
+    int32_t refine_stop_reason;
+    int32_t reserved;
+    double draft_ms;
+    double refine_ms;
+} dlm_cascade_stats;
+
+size_t dlm_cascade_workspace_bytes(const dlm_config* drafter_cfg, const dlm_config* refiner_cfg, int32_t batch,
+                                   int32_t prompt_len, int32_t draft_len, int32_t block_len);
+dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                       const int32_t* d_prompt, int32_t* d_draft, int32_t block_len, int32_t steps_per_block,
+                       float draft_threshold, int32_t n_refine_steps, const dlm_edit_rule* rule, void* d_workspace,
+                       size_t workspace_bytes, void* hip_stream, dlm_cascade_stats* h_stats);
+
+/*
  * Test hooks (same kernels as dlm_refine_step, intermediate results exposed).
  *
  * dlm_debug_forward: forward over d_tokens without the reduction; writes the

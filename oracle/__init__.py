@@ -12,4 +12,4 @@ from .refine import (  # noqa: F401
     refine_ex, refine_local, refine_step, refine_step_ex,
     rms_norm, rope, route, softmax, swiglu,
 )
-from .draft import block_key_limit, draft, draft_forward_block, draft_select, draft_step  # noqa: F401
+from .draft import block_key_limit, cascade, draft, draft_forward_block, draft_select, draft_step  # noqa: F401

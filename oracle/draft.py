@@ -28,13 +28,16 @@ What is computed (paper: Sec. 3.3 "Block Autoregressive Diffusion", Sec. 4.1
   * Batches: all sequences share the block positions; a step runs over the
     whole batch and changes only sequences that still have masked slots in the
     block; the block ends when none has.
+  * Speculative correction (Sec. 4.3): a drafter drafts, a refiner (sharing the
+    vocabulary) refines the finished draft; the cost is K x T_d drafting passes
+    plus T_r refinement passes (Sec. 4.2).
 """
 
 from __future__ import annotations
 
 import numpy as np
 
-from .refine import forward, lm_head_reduce
+from .refine import forward, lm_head_reduce, refine_ex
 
 
 def block_key_limit(prompt_len: int, seq_len: int, block_len: int) -> np.ndarray:
@@ -126,3 +129,12 @@ def draft(W, prompt: np.ndarray, draft_len: int, block_len: int, steps: int, tau
     out = tokens[:, P:]
     return out, {"steps_run": int(sum(block_steps)), "block_steps": block_steps,
                  "n_masked_left": int(np.sum(out == mask_id))}
+
+
+def cascade(W_draft, W_refine, prompt: np.ndarray, draft_len: int, block_len: int, steps: int, tau_draft: float,
+            n_refine: int, tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = True):
+    """Draft with W_draft, then refine_ex with W_refine on the finished draft
+    (no mask set).  Returns (refined draft, {"draft", "refine", "passes"})."""
+    d, ds = draft(W_draft, prompt, draft_len, block_len, steps, tau_draft, decide_bf16)
+    r, rs = refine_ex(W_refine, prompt, d, None, n_refine, tau_unmask, tau_edit, eos_id, decide_bf16)
+    return r, {"draft": ds, "refine": rs, "draft_tokens": d, "passes": ds["steps_run"] + rs["steps_run"]}

@@ -43,6 +43,18 @@ class DlmEditRule(ctypes.Structure):
                 ("eos_id", ctypes.c_int32)]
 
 
+class DlmCascadeStats(ctypes.Structure):
+    _fields_ = [("draft", DlmStats), ("refine", DlmStats), ("draft_passes", ctypes.c_int32),
+                ("refine_passes", ctypes.c_int32), ("refine_stop_reason", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("draft_ms", ctypes.c_double), ("refine_ms", ctypes.c_double)]
+
+    def as_dict(self):
+        return {"draft": self.draft.as_dict(), "refine": self.refine.as_dict(),
+                "draft_passes": int(self.draft_passes), "refine_passes": int(self.refine_passes),
+                "refine_stop_reason": int(self.refine_stop_reason), "draft_ms": float(self.draft_ms),
+                "refine_ms": float(self.refine_ms)}
+
+
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
 _F = ctypes.c_float
@@ -65,6 +77,9 @@ SIGNATURES = [
     ("dlm_draft", _I, [_P, _I, _I, _I, _P, _P, _I, _I, _F, _P, _SZ, _P, ctypes.POINTER(DlmStats),
                        ctypes.POINTER(_I)]),
     ("dlm_draft_step", _I, [_P, _I, _I, _I, _I, _I, _I, _F, _P, _P, _SZ, _P, _P, _P, _P, _P]),
+    ("dlm_cascade_workspace_bytes", _SZ, [_CFG, _CFG, _I, _I, _I, _I]),
+    ("dlm_cascade", _I, [_P, _P, _I, _I, _I, _P, _P, _I, _I, _F, _I, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
+                         ctypes.POINTER(DlmCascadeStats)]),
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
     ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),

@@ -15,6 +15,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <chrono>
 #include <string>
 #include <vector>
 
@@ -919,6 +920,42 @@ dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t dr
     HIP_TRY(hipStreamSynchronize(dr.st));
     tot.n_masked_left = fin.n_masked_left;
     if (h_stats) *h_stats = tot;
+    return DLM_OK;
+}
+
+size_t dlm_cascade_workspace_bytes(const dlm_config* drafter_cfg, const dlm_config* refiner_cfg, int32_t batch,
+                                   int32_t prompt_len, int32_t draft_len, int32_t block_len) {
+    const size_t a = dlm_draft_workspace_bytes(drafter_cfg, batch, prompt_len, draft_len, block_len);
+    const size_t b = dlm_workspace_bytes(refiner_cfg, batch, prompt_len, draft_len);
+    return a && b ? std::max(a, b) : 0;
+}
+
+dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                       const int32_t* d_prompt, int32_t* d_draft, int32_t block_len, int32_t steps_per_block,
+                       float draft_threshold, int32_t n_refine_steps, const dlm_edit_rule* rule, void* d_workspace,
+                       size_t workspace_bytes, void* hip_stream, dlm_cascade_stats* h_stats) {
+    if (!drafter || !refiner) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+    if (drafter->cfg.vocab != refiner->cfg.vocab || drafter->cfg.mask_id != refiner->cfg.mask_id)
+        return fail(DLM_ERR_INVALID_ARG, "drafter and refiner must share the vocabulary and the mask id");
+    if (n_refine_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_refine_steps < 0");
+    TRY(check_rule(refiner->cfg, rule));
+    if (workspace_bytes < dlm_cascade_workspace_bytes(&drafter->cfg, &refiner->cfg, batch, prompt_len, draft_len,
+                                                      block_len))
+        return fail(DLM_ERR_WORKSPACE, "workspace too small for the cascade");
+    using clk = std::chrono::steady_clock;
+    dlm_cascade_stats cs{};
+    const auto t0 = clk::now();
+    TRY(dlm_draft(drafter, batch, prompt_len, draft_len, d_prompt, d_draft, block_len, steps_per_block,
+                  draft_threshold, d_workspace, workspace_bytes, hip_stream, &cs.draft, nullptr));
+    const auto t1 = clk::now();              // dlm_draft returns with the draft written
+    TRY(dlm_refine_ex(refiner, batch, prompt_len, draft_len, d_prompt, d_draft, nullptr, n_refine_steps, rule,
+                      d_workspace, workspace_bytes, hip_stream, &cs.refine, &cs.refine_stop_reason));
+    const auto t2 = clk::now();              // and so does dlm_refine_ex
+    cs.draft_passes = cs.draft.steps_run;
+    cs.refine_passes = cs.refine.steps_run;
+    cs.draft_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+    cs.refine_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
+    if (h_stats) *h_stats = cs;
     return DLM_OK;
 }
 

@@ -288,6 +288,36 @@ class Refiner:
         return [(names[i].decode(), float(ms[i])) for i in range(n)]
 
 
+# ------------------------------------------------------------------ cascade
+
+_CASCADE_WS = {}
+
+
+def cascade(drafter: "Refiner", refiner: "Refiner", prompt: torch.Tensor, draft_len: int, block_len: int,
+            steps_per_block: int, draft_threshold: float, n_refine_steps: int, unmask_threshold: float,
+            edit_threshold: float, eos_id: int = -1):
+    """Draft with `drafter`, refine with `refiner` (dlm_cascade).  Returns
+    (refined draft [B, draft_len] int32, stats dict)."""
+    B, P = prompt.shape
+    key = (id(drafter), id(refiner), B, P, draft_len, block_len)
+    ws = _CASCADE_WS.get(key)
+    if ws is None:
+        n = refiner.lib.dlm_cascade_workspace_bytes(ctypes.byref(drafter.cfg), ctypes.byref(refiner.cfg), B, P,
+                                                    draft_len, block_len)
+        if n == 0:
+            raise ValueError(f"invalid cascade shape {key[2:]}")
+        ws = torch.empty(n, dtype=torch.uint8, device=refiner.device)
+        _CASCADE_WS[key] = ws
+    out = torch.empty(B, draft_len, dtype=torch.int32, device=refiner.device)
+    rule = _lib.DlmEditRule(float(unmask_threshold), float(edit_threshold), int(eos_id))
+    st = _lib.DlmCascadeStats()
+    check(refiner.lib.dlm_cascade(drafter._handle, refiner._handle, B, P, draft_len, _ptr(prompt) if P else None,
+                                  out.data_ptr(), block_len, steps_per_block, float(draft_threshold),
+                                  n_refine_steps, ctypes.byref(rule), ws.data_ptr(), ws.numel(), refiner.stream,
+                                  ctypes.byref(st)), "dlm_cascade")
+    return out, st.as_dict()
+
+
 # ------------------------------------------------------------------ GEMM hook
 
 def debug_gemm(a: torch.Tensor, b: torch.Tensor, tile=(256, 256)) -> torch.Tensor:

@@ -231,3 +231,44 @@ def test_draft_step_small_moe(small):
     # the [MASK] rows enter layer 0 identical, so they share one router gap and
     # are exempt together when it is small; the real-token rows remain
     assert ok.sum() >= b // 4
+
+
+def test_cascade_tiny(tiny_sharp):
+    """Two-model cascade (Sec. 4.3; cost K x T_d + T_r, Sec. 4.2): a one-layer
+    drafter (other seed, same vocabulary) drafts, the two-layer refiner refines.
+    dlm_cascade equals dlm_draft then dlm_refine_ex bit for bit, with their
+    pass counts; the drafter's trajectory agrees with the oracle step by step
+    (as above) and the refiner's first pass on the GPU's draft with the
+    oracle's pass at non-exempt positions.  Models of different vocabularies
+    are refused."""
+    import oracle
+    from paper_2608_02625_amd import DlmError, Refiner, cascade
+    torch = _torch()
+    w, s, Rl, Wl = tiny_sharp
+    ds = s.replace(n_layers=1)
+    Rs, Ws = Refiner(ds.as_dict(), 3), oracle.OracleWeights(ds, 3)
+    prompt = _prompts(s.vocab, 2, 24, 11)
+    P, D, b, T, td, n_ref, tu, te = 24, 48, 16, 4, 0.25, 4, 0.25, 0.625
+    out, st = cascade(Rs, Rl, _cuda_i32(prompt), D, b, T, td, n_ref, tu, te)
+    d, dst = Rs.draft(_cuda_i32(prompt), D, b, T, td)
+    r = d.clone()
+    _, rst = Rl.refine_ex(_cuda_i32(prompt), r, None, n_ref, tu, te)
+    log(f"[cascade tiny] {st}")
+    assert np.array_equal(_np(out), _np(r))
+    assert st["draft_passes"] == dst["steps_run"] == sum(dst["block_steps"])
+    assert st["refine_passes"] == rst["steps_run"] and st["refine_stop_reason"] == rst["stop_reason"]
+    assert st["draft_ms"] > 0 and st["refine_ms"] > 0
+    # the drafter's own trajectory against the oracle
+    _trajectory(Rs, Ws, ds, prompt, D, b, T, td, MARGIN * s.lm_head_scale, "cascade drafter")
+    # the refiner's first pass on the GPU's draft
+    tok = np.concatenate([prompt, _np(d)], 1).astype(np.int32)
+    ref_next, info = oracle.refine_step_ex(Wl, tok, P, tu, te)
+    g = _cuda_i32(tok)
+    Rl.refine_step_ex(g, P, tu, te)
+    thr = np.where(tok[:, P:] == s.mask_id, tu, te)
+    ex = (info["margin"] <= MARGIN * s.lm_head_scale) | (np.abs(info["conf"] - thr) <= CONF_TOL)
+    assert np.array_equal(_np(g)[:, P:][~ex], ref_next[:, P:][~ex])
+    assert int((~ex).sum()) > 0
+    other = Refiner(s.replace(vocab=4096).as_dict(), 0)
+    with pytest.raises(DlmError):
+        cascade(other, Rl, _cuda_i32(prompt), D, b, T, td, n_ref, tu, te)

@@ -145,3 +145,27 @@ def test_draft_forward_block_is_prefix_forward(tiny):
     red = lm_head_reduce(W, x[0, P + b:P + 2 * b])
     assert np.array_equal(info["top1"][0], red["top1"])
     np.testing.assert_allclose(info["conf"][0], red["conf"], rtol=1e-12)
+
+
+def test_cascade_pass_accounting(tiny):
+    """Sec. 4.2's cost K x T_d + T_r: with pure quota pacing every block uses
+    its T_d steps; zero refinement passes return the draft; the refine stage
+    is refine_ex on the finished draft; a refiner identical to the drafter
+    still runs (flash-flash, Sec. 4.3)."""
+    from oracle.draft import cascade
+    from oracle.refine import refine_ex
+    w, W = tiny
+    prompt, _, _ = make_inputs(w)
+    pr = prompt[:, :16]
+    Ws = oracle.OracleWeights(w.model.replace(n_layers=1), 3)
+    K, Td, b = 3, 4, 8
+    r0, st0 = cascade(Ws, W, pr, K * b, b, Td, 2.0, 0, 0.5, 0.5)
+    d, _ = draft(Ws, pr, K * b, b, Td, 2.0)
+    assert np.array_equal(r0, d) and st0["passes"] == K * Td and st0["refine"]["steps_run"] == 0
+    r, st = cascade(Ws, W, pr, K * b, b, Td, 2.0, 3, 0.2, 0.2)
+    ref, rst = refine_ex(W, pr, d, None, 3, 0.2, 0.2)
+    assert np.array_equal(r, ref) and st["passes"] == K * Td + rst["steps_run"]
+    assert 1 <= rst["steps_run"] <= 3
+    same, sst = cascade(W, W, pr, K * b, b, Td, 0.3, 2, 0.2, 0.2)
+    assert sst["draft"]["steps_run"] <= K * Td and sst["passes"] == sst["draft"]["steps_run"] + \
+        sst["refine"]["steps_run"]

@@ -97,6 +97,12 @@ MODELS = {
     "mini_moe": ModelShape(n_layers=20, d_model=2048, n_heads=16, n_kv_heads=4, head_dim=128,
                            ffn_dim=0, n_experts=64, top_k=8, expert_ffn_dim=1024,
                            n_shared_experts=1, vocab=157184),
+    # Drafter for the two-model cascade with mini_moe as refiner (same
+    # 157184-token vocabulary): 8 layers, d 1024, 16 heads of 64 with 4 KV
+    # heads, 32 experts top-4 (width 512) + 1 shared.
+    "mini_drafter": ModelShape(n_layers=8, d_model=1024, n_heads=16, n_kv_heads=4, head_dim=64,
+                               ffn_dim=0, n_experts=32, top_k=4, expert_ffn_dim=512,
+                               n_shared_experts=1, vocab=157184),
     # Flash-scale 8-layer slice: d 4096, 32 heads of 128 with 8 KV heads,
     # 256 experts top-8 (width 1536) + 1 shared.
     "flash_slice": ModelShape(n_layers=8, d_model=4096, n_heads=32, n_kv_heads=8, head_dim=128,
