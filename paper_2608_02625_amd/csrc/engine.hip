@@ -377,8 +377,10 @@ dlm_status run_layer(Ctx& x, int l) {
         a.ldo = d;
         const int64_t big_tiles = (int64_t)((x.T + 255) / 256) * ((d + 255) / 256);
         a.variant = big_tiles >= 128 ? 11 : 0;
-        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, a.variant != 0 || x.T >= 4096 ? 256 : 128,
-                 a.variant != 0 ? 256 : 128, 0));
+        // up to 1024 rows (drafting windows): 128 x 64 tiles, twice the workgroups of 128 x 128
+        const int obm = a.variant != 0 || x.T >= 4096 ? 256 : 128;
+        const int obn = a.variant != 0 ? 256 : x.T <= 1024 ? 64 : 128;
+        TRY(gemm(x, "gemm_o", a, EPI_RESID, false, obm, obn, 0));
     }
     LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g2), h, x.T, d, c.norm_eps, x.st));
     if (c.n_experts == 0) {

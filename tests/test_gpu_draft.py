@@ -272,3 +272,43 @@ def test_cascade_tiny(tiny_sharp):
     other = Refiner(s.replace(vocab=4096).as_dict(), 0)
     with pytest.raises(DlmError):
         cascade(other, Rl, _cuda_i32(prompt), D, b, T, td, n_ref, tu, te)
+
+
+def test_draft_mini_moe_properties():
+    """The mini-scale MoE workload at full size, in the benchmark's drafting
+    configuration (B 8, prompt 256, 384 positions, b64, s16, t0.25), through
+    properties that hold at any size: the whole draft is bit-identical run to
+    run; drafting 128 positions gives the first two blocks of the 384-position
+    draft (later blocks are invisible); with the threshold above 1 every step
+    of block 0 unmasks exactly ceil(n / r) slots per sequence; a threshold <= 0
+    fills every block in one step; no [MASK] is left."""
+    need_gpu()
+    from paper_2608_02625_amd import Refiner
+    torch = _torch()
+    w = WORKLOADS["mini_moe"]
+    s = w.model
+    log("[draft mini_moe] building model on cuda:0")
+    R = Refiner(s.as_dict(), w.weight_seed)
+    prompt, _, _ = make_inputs(w)
+    B, P, D = w.batch, w.prompt_len, w.draft_len
+    pr = _cuda_i32(prompt)
+    a, sa = R.draft(pr, D, 64, 16, 0.25)
+    b_, sb = R.draft(pr, D, 64, 16, 0.25)
+    log(f"[draft mini_moe] {sa}")
+    assert np.array_equal(_np(a), _np(b_)) and sa == sb
+    assert sa["n_masked_left"] == int((_np(a) == s.mask_id).sum()) == 0
+    assert all(1 <= t <= 16 for t in sa["block_steps"]) and sa["steps_run"] == sum(sa["block_steps"])
+    short, _ = R.draft(pr, 128, 64, 16, 0.25)
+    assert np.array_equal(_np(short), _np(a)[:, :128])
+    g = _cuda_i32(np.concatenate([prompt, np.full((B, D), s.mask_id, dtype=np.int32)], 1))
+    stats = torch.zeros(4, dtype=torch.int32, device="cuda")
+    left = 64
+    for t in range(4):
+        R.draft_step(g, P, 64, 0, 16 - t, 2.0, stats=stats)
+        st = _np(stats).tolist()
+        quota = -(-left // (16 - t))
+        assert st[0] == B * quota and st[2] == B * (left - quota), (t, st)
+        left -= quota
+    z, sz = R.draft(pr, D, 64, 16, 0.0)
+    log(f"[draft mini_moe] threshold 0: {sz}")
+    assert sz["block_steps"] == [1] * 6 and sz["n_masked_left"] == 0
