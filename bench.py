@@ -212,9 +212,10 @@ def cpu_baseline_draft(w, block, steps_avg):
 
 def bench_draft(args, w, R, prompt_np):
     """Block-AR drafting: a step is one whole draft of the batch (prefill of
-    the prompt, every block's denoising steps, the K/V commit of each finished
-    block).  The dominant kernel, the routed-expert gate/up GEMM of a block
-    window, streams every expert's weights once per launch: HBM-bound."""
+    the prompt, then every block's denoising steps; the first step of a block
+    also commits the previous block's K/V).  The dominant kernel, the
+    routed-expert gate/up GEMM of a block window, streams every expert's
+    weights once per launch: HBM-bound."""
     import numpy as np
     import torch
     shape = w.model
@@ -242,21 +243,27 @@ def bench_draft(args, w, R, prompt_np):
     n_blocks = -(-D // b)
     steps_run = stats[-1]["steps_run"]
     L = shape.n_layers
-    # per draft: prefill (layers 0..L-2 reach the experts), steps x L, commits x (L-1)
-    per_call = (L - 1 if P else 0) + steps_run * L + (n_blocks - 1) * (L - 1)
+    # per draft: prefill (layers 0..L-2 reach the experts), then steps x L
+    per_call = (L - 1 if P else 0) + steps_run * L
     assert len(launches) == per_call * args.steps, (len(launches), per_call)
     win = []
     for c in range(args.steps):
         seg = launches[c * per_call:(c + 1) * per_call]
         win.extend(seg[(L - 1 if P else 0):])                 # block windows only
     k_avg_ms = float(np.mean(win))
-    T = B * b
     G = shape.n_experts + shape.n_shared_experts
-    rows = T * shape.top_k + T * shape.n_shared_experts
     F, d = shape.expert_ffn_dim, shape.d_model
-    k_bytes = G * 2 * F * d * 2 + rows * d * 2 + rows * F * 2    # every expert's weights, gathered rows, output
+
+    def gu_bytes(T):                 # every expert's weights, gathered rows, output
+        rows = T * (shape.top_k + shape.n_shared_experts)
+        return G * 2 * F * d * 2 + rows * d * 2 + rows * F * 2
+
+    # the first step of blocks 1.. carries two blocks of rows
+    n_two = (n_blocks - 1) * L
+    n_one = steps_run * L - n_two
+    k_bytes = (n_one * gu_bytes(B * b) + n_two * gu_bytes(2 * B * b)) / (n_one + n_two)
     achieved = k_bytes / (k_avg_ms * 1e-3) / 1e9
-    passes = (1 if P else 0) + steps_run + n_blocks - 1
+    passes = (1 if P else 0) + steps_run
     out = {
         "metric": f"drafted positions/sec per block-AR draft (b{b}, s{s}, t{tau})",
         "value": B * D / (ms_draft * 1e-3), "unit": "drafted positions/s", "n_gpus": 1, "steps": args.steps,

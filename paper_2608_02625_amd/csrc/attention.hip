@@ -9,7 +9,10 @@
 // the Sq rows of one window (the prompt, or one block) and the keys are the
 // first n_keys rows of a longer per-layer K/V cache of Skv rows (everything up
 // to the window's end).  Every window query sees exactly those keys, which is
-// the block-causal mask for a window that is one block or the prompt.
+// the block-causal mask for a window that is one block or the prompt.  A
+// window may also hold the finished block before the current one: its first
+// q_split query rows then see only the first n_keys_lo keys (up to their own
+// block's end), the others all n_keys.
 //
 // One workgroup = 4 waves = 128 queries of one (batch, head); each wave owns 32
 // queries.  Per 64-key tile, K [64 keys][hd] and V^T [hd][64 keys] are copied
@@ -56,8 +59,8 @@ __device__ __forceinline__ int chunk_key(int row) {
 template <int HD>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
                                                    const bf16_t* Vt, bf16_t* __restrict__ O, int Sq, int Skv,
-                                                   int n_keys, int H, int KV, float scale_log2, uint32_t k_bytes,
-                                                   uint32_t v_bytes) {
+                                                   int n_keys, int q_split, int n_keys_lo, int H, int KV,
+                                                   float scale_log2, uint32_t k_bytes, uint32_t v_bytes) {
     using C = AttnCfg<HD>;
     __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
 
@@ -66,6 +69,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int kvh = h / (H / KV);
     const int q = qb * 128 + wave * 32 + j;
+    const int lim = q < q_split ? n_keys_lo : n_keys;   // keys this lane's query sees
     const int VS = vt_stride(Skv);
     const int wv = wave;
 
@@ -157,12 +161,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
                 st[c] = mfma32x32x16(kf, qf[ks], st[c]);
             }
         }
-        if (k0 + C::KEYS > n_keys) {                // last tile: keys past n_keys are not visible
+        if (k0 + C::KEYS > lim) {                   // keys past the lane's limit are not visible
 #pragma unroll
             for (int c = 0; c < 2; ++c)
 #pragma unroll
                 for (int e = 0; e < 16; ++e)
-                    if (k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= n_keys) st[c][e] = -INFINITY;
+                    if (k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= lim) st[c][e] = -INFINITY;
         }
         float mt = -INFINITY;
 #pragma unroll
@@ -231,18 +235,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 }  // namespace
 
 hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, bf16_t* o, int B,
-                            int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st) {
+                            int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st, int q_split,
+                            int n_keys_lo) {
     if (Sq <= 0 || n_keys <= 0 || n_keys > Skv) return hipErrorInvalidValue;
+    if (q_split < 0 || q_split > Sq || (q_split > 0 && (n_keys_lo < 1 || n_keys_lo > n_keys)))
+        return hipErrorInvalidValue;
     const dim3 grid((Sq + 127) / 128, H, B);
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     // byte sizes of the K buffer (with its one-tile tail) and of V^T
     const int64_t kb = ((int64_t)B * KV * Skv + 64) * hd * 2, vb = (int64_t)B * KV * hd * vt_stride(Skv) * 2;
     if (kb >= 0x7fffffff || vb >= 0x7fffffff) return hipErrorInvalidValue;   // 32-bit buffer offsets
     if (hd == 128)
-        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, H, KV,
+        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, q_split, n_keys_lo, H, KV,
                            scale_log2, (uint32_t)kb, (uint32_t)vb);
     else if (hd == 64)
-        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, H, KV,
+        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, q_split, n_keys_lo, H, KV,
                            scale_log2, (uint32_t)kb, (uint32_t)vb);
     else
         return hipErrorInvalidValue;

@@ -266,6 +266,7 @@ struct Ctx {
     size_t kc_layer = 0, vc_layer = 0;  // elements per layer
     const float2* rope_all = nullptr;   // RoPE table of all kv_seq positions
     bool kv_only = false;               // stop after the last layer's K/V (cache commit)
+    int att_split = 0, att_keys_lo = 0;  // window rows below att_split see only att_keys_lo keys
     template <class Tp>
     Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
     const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
@@ -367,7 +368,8 @@ dlm_status run_layer(Ctx& x, int l) {
     if (x.kv_only && l + 1 == c.n_layers) return DLM_OK;    // the cache holds this window's K/V now
     {
         prof_begin(x, "attention");
-        hipError_t e = launch_attention(q, k, v, attn, x.B, x.S, kvS, x.q0 + x.S, H, KV, hd, x.st);
+        hipError_t e = launch_attention(q, k, v, attn, x.B, x.S, kvS, x.q0 + x.S, H, KV, hd, x.st, x.att_split,
+                                        x.att_keys_lo);
         prof_end(x, "attention");
         if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("attention: ") + hipGetErrorString(e));
     }
@@ -529,7 +531,7 @@ struct DraftPlan {
 
 DraftPlan plan_draft(const dlm_config& c, int B, int P, int D, int blk) {
     DraftPlan p;
-    p.rows = std::max(P, std::min(blk, D));
+    p.rows = std::max(P, std::min(2 * blk, D));       // a block window may carry the block before it
     p.w = plan_workspace(c, B, 0, p.rows);
     size_t total = p.w.total;
     auto add = [&](int64_t bytes) {
@@ -592,11 +594,20 @@ struct Drafter {
     int32_t* counters() const { return reinterpret_cast<int32_t*>(ws + p.w.counters); }
 
     // Forward of one window of the token state: all layers' K/V of its rows go
-    // into the caches; with head, also the top-1 / confidence of its rows.
-    dlm_status run(const int32_t* tokens, int c0, int L, bool head) const {
+    // into the caches; with head, also the top-1 / confidence of its rows from
+    // row `lead` on.  The first `lead` rows are a finished block carried along
+    // to commit its K/V: they see keys only up to their own end.
+    dlm_status run(const int32_t* tokens, int c0, int L, bool head, int lead = 0) const {
         Ctx x = window(c0, L);
         const dlm_config& c = m->cfg;
         x.kv_only = !head;
+        if (lead) {
+            x.P = lead;
+            x.D = L - lead;
+            x.R = B * (L - lead);
+            x.att_split = lead;
+            x.att_keys_lo = c0 + lead;
+        }
         int32_t* wtok = x.at<int32_t>(p.wtok);
         LAUNCH(x, "window_gather", launch_window_gather(tokens, wtok, B, S, c0, L, st));
         LAUNCH(x, "embed", launch_embed(wtok, x.wt(m->plan.emb), x.at<float>(p.w.x), x.T, c.d_model, c.vocab, st));
@@ -624,10 +635,16 @@ struct Drafter {
     int block_rows(int k) const { return std::min(blk, S - block_start(k)); }
 
     // One denoising step on block k: forward of the block's window, then the
-    // unmasking.  counters: [0] unmasked, [2] masked left in the block, [3] = 1.
-    dlm_status step(int32_t* tokens, int k, float tau, int steps_left, int32_t* top1_out, float* conf_out) const {
+    // unmasking.  With with_prev, the window also carries block k-1 (finished,
+    // its K/V not yet in the caches), which commits it in the same pass.
+    // counters: [0] unmasked, [2] masked left in the block, [3] = 1.
+    dlm_status step(int32_t* tokens, int k, float tau, int steps_left, int32_t* top1_out, float* conf_out,
+                    bool with_prev = false) const {
         const int c0 = block_start(k), L = block_rows(k);
-        TRY(run(tokens, c0, L, true));
+        if (with_prev)
+            TRY(run(tokens, c0 - blk, blk + L, true, blk));
+        else
+            TRY(run(tokens, c0, L, true));
         Ctx x = window(c0, L);
         launch_zero_i32(counters(), 4, st);
         prof_begin(x, "draft_select");
@@ -901,7 +918,8 @@ dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t dr
     for (int k = 0; k < n_blocks; ++k) {
         int used = 0;
         for (int t = 0; t < steps_per_block; ++t) {
-            TRY(dr.step(tokens, k, threshold, steps_per_block - t, nullptr, nullptr));
+            // the first step of a block also commits the previous block's K/V
+            TRY(dr.step(tokens, k, threshold, steps_per_block - t, nullptr, nullptr, t == 0 && k > 0));
             int32_t c[4] = {};
             HIP_TRY(hipMemcpyAsync(c, dr.counters(), sizeof(c), hipMemcpyDeviceToHost, dr.st));
             HIP_TRY(hipStreamSynchronize(dr.st));
@@ -911,7 +929,6 @@ dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t dr
         }
         tot.steps_run += used;
         if (h_block_steps) h_block_steps[k] = used;
-        if (k + 1 < n_blocks) TRY(dr.run(tokens, dr.block_start(k), dr.block_rows(k), false));   // commit its K/V
     }
     launch_copy_draft_out(tokens, d_draft, batch, S, prompt_len, draft_len, dr.st);
     launch_zero_i32(dr.counters(), 4, dr.st);

@@ -73,8 +73,11 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, bool grouped, int bm, int bn,
 // Non-causal attention over Q [B][H][S][hd], K, V [B][KV][S][hd]; O [B*S][H*hd] bf16.
 // Draft windows: Q holds Sq rows per sequence, K and V^T hold Skv rows per
 // sequence of which the first n_keys are visible (n_keys <= Skv); O [B*Sq][H*hd].
+// With q_split > 0 the first q_split query rows see only the first n_keys_lo
+// keys (1 <= n_keys_lo <= n_keys).
 hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* v, bf16_t* o, int B,
-                            int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st);
+                            int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st, int q_split = 0,
+                            int n_keys_lo = 0);
 
 // ----------------------------------------------------------------- elementwise.hip
 void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
