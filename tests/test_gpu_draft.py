@@ -312,3 +312,16 @@ def test_draft_mini_moe_properties():
     z, sz = R.draft(pr, D, 64, 16, 0.0)
     log(f"[draft mini_moe] threshold 0: {sz}")
     assert sz["block_steps"] == [1] * 6 and sz["n_masked_left"] == 0
+
+
+def test_draft_tiny_extreme_blocks(tiny_sharp):
+    """Degenerate and maximum block sizes: blocks of one token (causal over the
+    response, one step each) and blocks of 1024 (the largest the unmasking
+    kernel ranks at once; the second block's window carries 2 x 1024 rows),
+    with a ragged last block."""
+    w, s, R, W = tiny_sharp
+    m = MARGIN * s.lm_head_scale
+    _, bs = _trajectory(R, W, s, _prompts(s.vocab, 1, 12, 21), 6, 1, 1, 0.25, m, "tiny block 1")
+    assert bs == [1] * 6
+    _, bs = _trajectory(R, W, s, _prompts(s.vocab, 1, 16, 22), 1100, 1024, 2, 0.25, m, "tiny block 1024")
+    assert len(bs) == 2
