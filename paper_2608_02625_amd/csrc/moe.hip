@@ -8,23 +8,29 @@
 
 namespace {
 
-// XOR key of the 16-byte chunks of a 128-byte LDS row: 32 consecutive rows
-// read at one logical chunk hit distinct banks.
-__device__ __forceinline__ int rkey(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+// XOR key of the 16-byte chunks of an LDS row of CPR chunks (8, 16 or 32):
+// a fragment read of 32 consecutive rows at one logical chunk hits distinct
+// banks (with 16 or more chunks per row the low four row bits suffice).
+template <int CPR>
+__device__ __forceinline__ int rkey(int row) {
+    if constexpr (CPR >= 16) return row & 15;
+    else return (row & 7) ^ ((row >> 3) & 1);
+}
 
 // Router + top-k for 32 tokens per workgroup (8 waves).
 // z^T[e][t] = sum_c Wr[e][c] h[t][c] on v_mfma_f32_32x32x16_bf16 with experts
-// as rows (NB <= 8 blocks of 32) and tokens as columns.  K advances 64
-// columns at a time through 3 to 8 LDS stages that the waves fill with buffer
-// loads straight from global memory (whole 128-byte row segments, 16-byte
-// chunks XOR-swizzled), so every byte of h and Wr is fetched once per
-// workgroup in full cache lines.  Each expert block's 16-wide K steps are
-// dealt round-robin to 8 / NB waves and the parts are added in a fixed order.
+// as rows (NB <= 8 blocks of 32) and tokens as columns.  K advances ROWB / 2
+// columns at a time (64, 128 or 256) through 3 to 8 LDS stages that the
+// waves fill with buffer loads straight from global memory (whole ROWB-byte
+// row segments, 16-byte chunks XOR-swizzled), so every byte of h and Wr is
+// fetched once per workgroup in full cache lines.  Each expert block's
+// 16-wide K steps are dealt round-robin to 8 / NB waves and the parts are
+// added in a fixed order.
 // Each wave then selects for 4 tokens; lane r < k records selection r with its
 // rank among this workgroup's selections of the same expert (LDS counter), and
 // the workgroup's per-expert counts go to wg_counts[E][workgroup].  Ranks only
 // order rows inside an expert's group.
-template <int NB>
+template <int NB, int ROWB>
 __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restrict__ h, const bf16_t* __restrict__ Wr,
                                                          int T, int d, int E, int k, int32_t* __restrict__ ids,
                                                          float* __restrict__ wts, int32_t* __restrict__ pos,
@@ -34,12 +40,15 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
     constexpr int KSPLIT = NW / NB;                  // waves sharing an expert block
     constexpr int EP = NB * 32;                      // padded expert count (LDS row)
     constexpr int ZROW = EP + 4;                     // row stride: 16-byte aligned, 4 banks of skew
-    constexpr int ROWB = 128;                        // bytes per LDS row: 64 K columns
+    constexpr int CPR = ROWB / 16;                   // 16-byte chunks per LDS row
+    constexpr int RPB = 1024 / ROWB;                 // rows per 1 KB copy block
+    constexpr int HB = 32 / RPB;                     // copy blocks of token rows
+    constexpr int KSTEPS = ROWB / 32;                // 16-wide K steps per chunk
     constexpr int H_BYTES = 32 * ROWB, STAGE = H_BYTES + EP * ROWB;
     // Stages: as many as fit in 96 KB (3 to 8), so that several K chunks
     // are in flight while one is multiplied.
     constexpr int NS = 96 * 1024 / STAGE < 3 ? 3 : (96 * 1024 / STAGE > 8 ? 8 : 96 * 1024 / STAGE);
-    constexpr int NBLK = STAGE / 1024;               // 1 KB copy blocks per stage (8 rows each)
+    constexpr int NBLK = STAGE / 1024;               // 1 KB copy blocks per stage (RPB rows each)
     constexpr int NI = (NBLK + NW - 1) / NW;         // copies per wave and stage (the last block repeats)
     constexpr int ZBYTES = KSPLIT * 32 * ZROW * 4 + 32 * EP * 8;
     constexpr int LBYTES = NS * STAGE > ZBYTES ? NS * STAGE : ZBYTES;
@@ -57,8 +66,8 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
     const int blk0 = wave / KSPLIT, kc = wave % KSPLIT;
     for (int e = threadIdx.x; e < EP; e += NW * 64) lcnt[e] = 0;
 
-    // Copy block q of a stage: q < 4 holds token rows 8q .. 8q+7 of h, the
-    // others expert rows of Wr (rows past T or E repeat the last one).
+    // Copy block q of a stage: q < HB holds token rows RPB q .. RPB q + RPB - 1
+    // of h, the others expert rows of Wr (rows past T or E repeat the last one).
     const buf_rsrc_t h_rsrc = make_rsrc(h), w_rsrc = make_rsrc(Wr);
     uint32_t off[NI];
     bool is_h[NI];
@@ -66,17 +75,17 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
 #pragma unroll
     for (int p = 0; p < NI; ++p) {
         const int q = min(wave * NI + p, NBLK - 1);
-        const int r8 = lane >> 3, pc = lane & 7;
-        is_h[p] = q < 4;
-        const int row = is_h[p] ? q * 8 + r8 : (q - 4) * 8 + r8;
+        const int rr = lane / CPR, pc = lane % CPR;
+        is_h[p] = q < HB;
+        const int row = is_h[p] ? q * RPB + rr : (q - HB) * RPB + rr;
         const int64_t grow = is_h[p] ? min(t0 + row, T - 1) : min(row, E - 1);
-        off[p] = (uint32_t)(grow * d * 2) + (uint32_t)((pc ^ rkey(row)) * 16);
+        off[p] = (uint32_t)(grow * d * 2) + (uint32_t)((pc ^ rkey<CPR>(row)) * 16);
         dst[p] = q * 1024;
     }
     const lds_ptr_t lds = (lds_ptr_t)smem;
     typedef __attribute__((address_space(3))) char lds_char;
     typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
-    auto issue = [&](int c, int stage) {             // K columns 64c .. 64c+63 into a stage
+    auto issue = [&](int c, int stage) {             // K chunk c (ROWB / 2 columns) into a stage
 #pragma unroll
         for (int p = 0; p < NI; ++p)
             lds_dma16_buf(is_h[p] ? h_rsrc : w_rsrc, off[p], c * ROWB, (lds_ptr_t)((lds_char*)lds + stage * STAGE + dst[p]));
@@ -85,8 +94,8 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
     f32x16 acc;
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-    const int nk = d / 64;
-    const int hfrag = j * ROWB, wfrag = H_BYTES + (blk0 * 32 + j) * ROWB, key = rkey(j);
+    const int nk = d / (ROWB / 2);
+    const int hfrag = j * ROWB, wfrag = H_BYTES + (blk0 * 32 + j) * ROWB, key = rkey<CPR>(j);
 #pragma unroll
     for (int s = 0; s < NS; ++s) issue(min(s, nk - 1), s);
     for (int c = 0; c < nk; ++c) {
@@ -98,8 +107,8 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
         if (c > 0) issue(min(c + NS - 1, nk - 1), (c + NS - 1) % NS);
         const int sb = (c % NS) * STAGE;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            if ((c * 4 + ks) % KSPLIT != kc) continue;   // wave-uniform
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            if ((c * KSTEPS + ks) % KSPLIT != kc) continue;   // wave-uniform
             const int co = ((2 * ks + g) ^ key) << 4;
             const bf16x8 wf = *(lds_frag*)((lds_char*)lds + sb + wfrag + co);
             const bf16x8 hf = *(lds_frag*)((lds_char*)lds + sb + hfrag + co);
@@ -336,20 +345,46 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
     if (g_next) rms_store_row(xr, g_next, h_next + (int64_t)t * d, d, block_rms_scale(ss, d, eps));
 }
 
+template <int NB>
+void launch_router_nb(int rowb, dim3 grid, hipStream_t st, const bf16_t* h, const bf16_t* Wr, int T, int d, int E,
+                      int k, int32_t* ids, float* w, int32_t* pos, int32_t* wg_counts) {
+    if constexpr (NB <= 2) {
+        if (rowb == 512) {
+            hipLaunchKernelGGL((router_topk_kernel<NB, 512>), grid, dim3(512), 0, st, h, Wr, T, d, E, k, ids, w, pos,
+                               wg_counts);
+            return;
+        }
+    }
+    if constexpr (NB <= 4) {
+        if (rowb == 256) {
+            hipLaunchKernelGGL((router_topk_kernel<NB, 256>), grid, dim3(512), 0, st, h, Wr, T, d, E, k, ids, w, pos,
+                               wg_counts);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((router_topk_kernel<NB, 128>), grid, dim3(512), 0, st, h, Wr, T, d, E, k, ids, w, pos,
+                       wg_counts);
+}
+
 }  // namespace
 
 hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, int E, int k, int32_t* ids,
                               float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st) {
     if (E < 1 || E > 256 || k < 1 || k > 8 || k > E || d % 64 != 0 || T < 1) return hipErrorInvalidValue;
     const dim3 grid((T + 31) / 32), block(512);
+    // The widest K chunk (256, 128 or 64 columns: 512, 256 or 128-byte LDS
+    // rows, so the fewest stage barriers) that divides d and whose three
+    // stages fit in the LDS with the expert rows.
+    const int nb = E <= 32 ? 1 : E <= 64 ? 2 : E <= 128 ? 4 : 8;
+    const int rowb = nb <= 2 && d % 256 == 0 ? 512 : nb <= 4 && d % 128 == 0 ? 256 : 128;
     if (E <= 32)
-        hipLaunchKernelGGL(router_topk_kernel<1>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<1>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
     else if (E <= 64)
-        hipLaunchKernelGGL(router_topk_kernel<2>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<2>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
     else if (E <= 128)
-        hipLaunchKernelGGL(router_topk_kernel<4>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<4>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
     else
-        hipLaunchKernelGGL(router_topk_kernel<8>, grid, block, 0, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<8>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
     return hipGetLastError();
 }
 
