@@ -135,7 +135,9 @@ def cpu_baseline(w, layers_sample=1):
 
 def bench_local(args, w, R, tokens0):
     """Local refinement: a step is one pass over every chunk of the draft
-    (prompt ‖ chunk, the chunk at its positions in the full sequence)."""
+    (prompt ‖ chunk, the chunk at its positions in the full sequence).  The
+    roofline row is the gate/up expert GEMM of the chunk calls."""
+    import dataclasses
     import numpy as np
     import torch
     shape = w.model
@@ -150,14 +152,23 @@ def bench_local(args, w, R, tokens0):
 
     for _ in range(args.warmup):
         one_step()
+    kname = "gemm_expert_gate_up"
+    R.set_profiling(kname)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         one_step()
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    kt = [ms for (n, ms) in R.profile_read() if n == kname]
+    R.set_profiling(None)
     flops = sum(step_flops(shape, B, P, t.shape[1] - P) for _, t in chunks)
-    print(json.dumps({
+    # launches cycle through the chunks in order (one per layer per chunk call)
+    per_chunk = [kernel_flops(kname, shape, B, P, t.shape[1] - P) for _, t in chunks]
+    k_flops = float(np.mean([per_chunk[(i // shape.n_layers) % len(chunks)] for i in range(len(kt))]))
+    k_avg_ms = float(np.mean(kt))
+    achieved = k_flops / (k_avg_ms * 1e-3) / 1e12
+    out = {
         "metric": f"refined positions/sec per local refinement pass (chunks of {L})",
         "value": B * D / (ms_step * 1e-3), "unit": "refined positions/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
@@ -165,7 +176,16 @@ def bench_local(args, w, R, tokens0):
         "config": {"workload": w.name, "batch": B, "prompt_len": P, "draft_len": D, "local_span": L,
                    "chunks": len(chunks)},
         "step_mfma_frac": flops / (ms_step * 1e-3) / PEAK_BF16,
-    }), flush=True)
+        "roofline": {"kernel": kname + " (chunk calls)", "bound": "mfma", "achieved": achieved,
+                     "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": achieved / (PEAK_BF16 / 1e12),
+                     "traffic": None, "launches": len(kt), "avg_ms": k_avg_ms, "flops_per_launch": k_flops},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        cb = cpu_baseline(dataclasses.replace(w, draft_len=L))
+        cb["sample"] = f"one chunk call ({P} prompt + {L} chunk tokens): " + cb["sample"]
+        out["cpu_baseline"] = cb
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline_draft(w, block, steps_avg):
