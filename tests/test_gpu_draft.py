@@ -274,7 +274,16 @@ def test_cascade_tiny(tiny_sharp):
         cascade(other, Rl, _cuda_i32(prompt), D, b, T, td, n_ref, tu, te)
 
 
-def test_draft_mini_moe_properties():
+@pytest.fixture(scope="module")
+def mini():
+    need_gpu()
+    from paper_2608_02625_amd import Refiner
+    w = WORKLOADS["mini_moe"]
+    log("[draft mini_moe] building model on cuda:0")
+    return w, w.model, Refiner(w.model.as_dict(), w.weight_seed)
+
+
+def test_draft_mini_moe_properties(mini):
     """The mini-scale MoE workload at full size, in the benchmark's drafting
     configuration (B 8, prompt 256, 384 positions, b64, s16, t0.25), through
     properties that hold at any size: the whole draft is bit-identical run to
@@ -282,13 +291,8 @@ def test_draft_mini_moe_properties():
     draft (later blocks are invisible); with the threshold above 1 every step
     of block 0 unmasks exactly ceil(n / r) slots per sequence; a threshold <= 0
     fills every block in one step; no [MASK] is left."""
-    need_gpu()
-    from paper_2608_02625_amd import Refiner
     torch = _torch()
-    w = WORKLOADS["mini_moe"]
-    s = w.model
-    log("[draft mini_moe] building model on cuda:0")
-    R = Refiner(s.as_dict(), w.weight_seed)
+    w, s, R = mini
     prompt, _, _ = make_inputs(w)
     B, P, D = w.batch, w.prompt_len, w.draft_len
     pr = _cuda_i32(prompt)
@@ -325,3 +329,26 @@ def test_draft_tiny_extreme_blocks(tiny_sharp):
     assert bs == [1] * 6
     _, bs = _trajectory(R, W, s, _prompts(s.vocab, 1, 16, 22), 1100, 1024, 2, 0.25, m, "tiny block 1024")
     assert len(bs) == 2
+
+
+def test_cascade_mini_moe_full_size(mini):
+    """The benchmark's cascade at full size (mini_drafter drafts B 8 x 384 with
+    b64 s16 t0.25, the mini-scale MoE refines up to 4 passes at 0.20): equal
+    bit for bit to drafting then refining separately, with the pass counts
+    K x T_d + T_r of the two stages."""
+    from paper_2608_02625_amd import Refiner, cascade
+    from workloads import MODELS
+    w, s, R = mini
+    Rd = Refiner(MODELS["mini_drafter"].as_dict(), w.weight_seed + 1)
+    prompt, _, _ = make_inputs(w)
+    pr = _cuda_i32(prompt)
+    D = w.draft_len
+    out, st = cascade(Rd, R, pr, D, 64, 16, 0.25, 4, 0.2, 0.2)
+    d, dst = Rd.draft(pr, D, 64, 16, 0.25)
+    r = d.clone()
+    _, rst = R.refine_ex(pr, r, None, 4, 0.2, 0.2)
+    log(f"[cascade mini_moe] {st}")
+    assert np.array_equal(_np(out), _np(r))
+    assert st["draft_passes"] == dst["steps_run"] and st["refine_passes"] == rst["steps_run"]
+    assert st["draft_passes"] <= 6 * 16 and 1 <= st["refine_passes"] <= 4
+    assert int((_np(out) == s.mask_id).sum()) == 0
