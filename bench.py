@@ -392,6 +392,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mini_moe")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size")
     ap.add_argument("--kernel", default="gemm_expert_gate_up", help="kernel reported in roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-table", action="store_true", help="also time every kernel (separate pass)")
@@ -422,6 +423,9 @@ def main():
     from workloads import WORKLOADS, make_inputs
 
     w = WORKLOADS[args.workload]
+    if args.batch:
+        import dataclasses
+        w = dataclasses.replace(w, batch=args.batch)
     shape = w.model
     B, P, D = w.batch, w.prompt_len, w.draft_len
     torch.cuda.set_device(0)
