@@ -464,40 +464,51 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         } else if constexpr (EPI == EPI_LMHEAD) {
             // rows = vocabulary ids, cols = tokens.  Per token: (max, first argmax,
             // sum exp(z - max)) over each half tile's BM/2 vocabulary rows.
+            // Rows past the vocabulary exist only in the last tile: the checks
+            // are compiled in for that tile alone (a wave-uniform branch).  The
+            // exponent arguments are <= 0, so the hardware exp2 (no denormal
+            // rescaling) serves; terms below 2^-126 of the maximum vanish.
             SoftmaxPartial part[T::TN];
+            auto reduce = [&](auto checked) __attribute__((always_inline)) {
+                constexpr bool CHK = decltype(checked)::value;
 #pragma unroll
-            for (int j = 0; j < T::TN; ++j) {
-                float m = -INFINITY;
-                int idx = 0x7fffffff;
-#pragma unroll
-                for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-                        const float z = (v < rows) ? acc[i][j][e] : -INFINITY;
-                        if (z > m) {
-                            m = z;
-                            idx = v;
-                        }
-                    }
-                float s = 0.f;
-                if (m != -INFINITY) {
-                    const float ml = m * kLog2e;
+                for (int j = 0; j < T::TN; ++j) {
+                    float m = -INFINITY;
+                    int idx = 0x7fffffff;
 #pragma unroll
                     for (int i = 0; i < T::TM; ++i)
 #pragma unroll
                         for (int e = 0; e < 16; ++e) {
                             const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
-                            if (v < rows) s += exp2f(acc[i][j][e] * kLog2e - ml);
+                            const float z = (!CHK || v < rows) ? acc[i][j][e] : -INFINITY;
+                            if (z > m) {
+                                m = z;
+                                idx = v;
+                            }
                         }
+                    float s = 0.f;
+                    if (m != -INFINITY) {
+                        const float ml = m * kLog2e;
+#pragma unroll
+                        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                            for (int e = 0; e < 16; ++e) {
+                                const int v = m0 + lrow0 + i * 32 + 8 * (e >> 2) + (e & 3);
+                                if (!CHK || v < rows) s += __builtin_amdgcn_exp2f(acc[i][j][e] * kLog2e - ml);
+                            }
+                    }
+                    SoftmaxPartial p{m, idx, s};
+                    SoftmaxPartial q;
+                    q.m = __shfl_xor(p.m, 32, 64);
+                    q.idx = __shfl_xor(p.idx, 32, 64);
+                    q.s = __shfl_xor(p.s, 32, 64);
+                    part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
                 }
-                SoftmaxPartial p{m, idx, s};
-                SoftmaxPartial q;
-                q.m = __shfl_xor(p.m, 32, 64);
-                q.idx = __shfl_xor(p.idx, 32, 64);
-                q.s = __shfl_xor(p.s, 32, 64);
-                part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
-            }
+            };
+            if (m0 + BM <= rows)
+                reduce(std::false_type{});
+            else
+                reduce(std::true_type{});
             // One partial per (BM/2-row half tile, token): the two wave rows
             // (wm = 0, 1) write separately and the merge kernel combines them.
             if (lane < 32) {
