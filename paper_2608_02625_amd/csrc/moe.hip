@@ -45,9 +45,9 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
     constexpr int HB = 32 / RPB;                     // copy blocks of token rows
     constexpr int KSTEPS = ROWB / 32;                // 16-wide K steps per chunk
     constexpr int H_BYTES = 32 * ROWB, STAGE = H_BYTES + EP * ROWB;
-    // Stages: as many as fit in 96 KB (3 to 8), so that several K chunks
-    // are in flight while one is multiplied.
-    constexpr int NS = 96 * 1024 / STAGE < 3 ? 3 : (96 * 1024 / STAGE > 8 ? 8 : 96 * 1024 / STAGE);
+    // Stages: as many as fit in 150 KB (3 to 8), so that several K chunks
+    // are in flight while one is multiplied (the K loop is latency-bound).
+    constexpr int NS = 150 * 1024 / STAGE < 3 ? 3 : (150 * 1024 / STAGE > 8 ? 8 : 150 * 1024 / STAGE);
     constexpr int NBLK = STAGE / 1024;               // 1 KB copy blocks per stage (RPB rows each)
     constexpr int NI = (NBLK + NW - 1) / NW;         // copies per wave and stage (the last block repeats)
     constexpr int ZBYTES = KSPLIT * 32 * ZROW * 4 + 32 * EP * 8;
