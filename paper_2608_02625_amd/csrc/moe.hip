@@ -301,33 +301,40 @@ __global__ __launch_bounds__(256) void dispatch_scatter_kernel(const int32_t* __
 // x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[grp_off[E+s] + t], fixed order.
 // With g_next, also the next block's input norm h[t] = bf16(x[t] / rms * g_next)
 // (the same arithmetic, in the same order, as the stand-alone RMSNorm).
+// NR = k + n_shared rows per token, a compile-time count so that all of a
+// token's row loads are issued before the first is used.
+template <int NR>
 __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__ Y,
                                const int32_t* __restrict__ slot, const float* __restrict__ w,
                                const int32_t* __restrict__ grp_off, int k, int E, int n_shared,
                                int d, const bf16_t* __restrict__ g_next, bf16_t* __restrict__ h_next, float eps) {
     const int t = blockIdx.x;
-    int rows[9];
-    float wt[9];
-    int nrow = 0;
-    for (int j = 0; j < k; ++j) {
-        rows[nrow] = slot[(int64_t)t * k + j];
-        wt[nrow++] = w[(int64_t)t * k + j];
-    }
-    for (int s = 0; s < n_shared && nrow < 9; ++s) {
-        rows[nrow] = grp_off[E + s] + t;
-        wt[nrow++] = 1.f;
+    int rows[NR];
+    float wt[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        if (r < k) {
+            rows[r] = slot[(int64_t)t * k + r];
+            wt[r] = w[(int64_t)t * k + r];
+        } else {
+            rows[r] = grp_off[E + (r - k)] + t;
+            wt[r] = 1.f;
+        }
     }
     float* xr = x + (int64_t)t * d;
     float ss = 0.f;
     for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
+        u32x4 y[NR];
+#pragma unroll
+        for (int r = 0; r < NR; ++r) y[r] = *reinterpret_cast<const u32x4*>(Y + (int64_t)rows[r] * d + i);
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        for (int r = 0; r < nrow; ++r) {
-            const u32x4 y = *reinterpret_cast<const u32x4*>(Y + (int64_t)rows[r] * d + i);
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
             const float c = wt[r];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                acc[2 * q] += c * __uint_as_float(y[q] << 16);
-                acc[2 * q + 1] += c * __uint_as_float(y[q] & 0xffff0000u);
+                acc[2 * q] += c * __uint_as_float(y[r][q] << 16);
+                acc[2 * q + 1] += c * __uint_as_float(y[r][q] & 0xffff0000u);
             }
         }
         f32x4 a = *reinterpret_cast<const f32x4*>(xr + i);
@@ -404,6 +411,24 @@ hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
                     const int32_t* grp_off, int T, int k, int E, int n_shared, int d, const bf16_t* g_next,
                     bf16_t* h_next, float eps, hipStream_t st) {
-    hipLaunchKernelGGL(combine_kernel, dim3(T), dim3(256), 0, st, x, Y, slot, w, grp_off, k, E,
-                       n_shared, d, g_next, h_next, eps);
+    const int nr = k + std::min(n_shared, 9 - k);
+#define COMBINE_CASE(N)                                                                                    \
+    case N:                                                                                                \
+        hipLaunchKernelGGL(combine_kernel<N>, dim3(T), dim3(256), 0, st, x, Y, slot, w, grp_off, k, E, n_shared, d, \
+                           g_next, h_next, eps);                                                           \
+        break;
+    switch (nr) {
+        COMBINE_CASE(1)
+        COMBINE_CASE(2)
+        COMBINE_CASE(3)
+        COMBINE_CASE(4)
+        COMBINE_CASE(5)
+        COMBINE_CASE(6)
+        COMBINE_CASE(7)
+        COMBINE_CASE(8)
+        COMBINE_CASE(9)
+        default:
+            break;
+    }
+#undef COMBINE_CASE
 }
