@@ -336,3 +336,39 @@ def test_forward_small_moe(small):
         f"mismatches {mism}")
     assert eh <= HIDDEN_TOL and em <= HIDDEN_TOL
     assert mism == 0
+
+
+def test_refine_step_span_small_moe(small):
+    """Local refinement on the mixture-of-experts model: one pass over prompt ‖
+    a 64-token chunk that sits at draft offset 192 (RoPE positions shifted),
+    against the oracle's forward with the same positions.  Rows whose top-k
+    router gap is within 1e-2 at some layer are exempt (as in the forward
+    test); elsewhere top-1 exact outside the margin, confidences within 1e-2,
+    and the edits follow the rule on the GPU's own confidences."""
+    import oracle
+    torch = _torch()
+    w, s, R, W = small
+    prompt, draft, mask = make_inputs(w)
+    P, c0, L = w.prompt_len, 192, 64
+    chunk = np.where(mask, s.mask_id, draft)[:, c0:c0 + L]
+    tok = np.concatenate([prompt, chunk], 1).astype(np.int32)
+    pos = np.concatenate([np.arange(P), P + c0 + np.arange(L)])
+    x_ref, infos, _ = oracle.forward(W, tok, collect=True, positions=pos)
+    gap = np.min(np.stack([i["route_gap"] for i in infos]), axis=0)[0, P:]
+    red = oracle.lm_head_reduce(W, x_ref[0, P:])
+    g = _cuda_i32(tok)
+    t1 = torch.empty(L, dtype=torch.int32, device="cuda")
+    cf = torch.empty(L, dtype=torch.float32, device="cuda")
+    tau = 0.875
+    R.refine_step_span(g, P, c0, tau, tau, workspace_draft_len=w.draft_len, top1=t1, conf=cf)
+    gt1, gcf = _np(t1), _np(cf).astype(np.float64)
+    keep = gap > MARGIN
+    ok = keep & (red["margin"] > MARGIN)
+    log(f"[small_moe span] route-exempt {int((~keep).sum())}/{L}; conf err "
+        f"{np.max(np.abs(gcf[keep] - red['conf'][keep])):.2e}; top-1 checked {int(ok.sum())}/{L}")
+    assert np.array_equal(gt1[ok], red["top1"][ok])
+    assert np.max(np.abs(gcf[keep] - red["conf"][keep])) <= MARGIN
+    take = (gt1 != s.mask_id) & (gcf >= np.float32(tau))
+    assert np.array_equal(_np(g)[0, P:], np.where(take, gt1, chunk[0]))
+    assert np.array_equal(_np(g)[0, :P], prompt[0])
+    assert ok.sum() >= L // 4
