@@ -269,6 +269,9 @@ def test_cascade_tiny(tiny_sharp):
     ex = (info["margin"] <= MARGIN * s.lm_head_scale) | (np.abs(info["conf"] - thr) <= CONF_TOL)
     assert np.array_equal(_np(g)[:, P:][~ex], ref_next[:, P:][~ex])
     assert int((~ex).sum()) > 0
+    # no refinement passes: the cascade returns the draft
+    out0, st0 = cascade(Rs, Rl, _cuda_i32(prompt), D, b, T, td, 0, tu, te)
+    assert np.array_equal(_np(out0), _np(d)) and st0["refine_passes"] == 0
     other = Refiner(s.replace(vocab=4096).as_dict(), 0)
     with pytest.raises(DlmError):
         cascade(other, Rl, _cuda_i32(prompt), D, b, T, td, n_ref, tu, te)
@@ -352,3 +355,25 @@ def test_cascade_mini_moe_full_size(mini):
     assert st["draft_passes"] == dst["steps_run"] and st["refine_passes"] == rst["steps_run"]
     assert st["draft_passes"] <= 6 * 16 and 1 <= st["refine_passes"] <= 4
     assert int((_np(out) == s.mask_id).sum()) == 0
+
+
+def test_draft_flash_slice_properties():
+    """The flash-scale slice (256 experts top-8, 32 query and 8 key/value heads
+    of 128, d 4096) at its benchmark batch (16 x 256 prompt): drafting is
+    bit-identical run to run, the 64-position draft is the first block of the
+    384-position one, and nothing stays masked."""
+    need_gpu()
+    from paper_2608_02625_amd import Refiner
+    w = WORKLOADS["flash_slice"]
+    log("[draft flash_slice] building model on cuda:0")
+    R = Refiner(w.model.as_dict(), w.weight_seed)
+    prompt, _, _ = make_inputs(w)
+    pr = _cuda_i32(prompt)
+    a, sa = R.draft(pr, w.draft_len, 64, 16, 0.25)
+    b_, sb = R.draft(pr, w.draft_len, 64, 16, 0.25)
+    log(f"[draft flash_slice] {sa}")
+    assert np.array_equal(_np(a), _np(b_)) and sa == sb
+    short, _ = R.draft(pr, 64, 64, 16, 0.25)
+    assert np.array_equal(_np(short), _np(a)[:, :64])
+    assert sa["n_masked_left"] == 0
+    del R
