@@ -95,3 +95,15 @@ def test_errors_are_reported_without_gpu_work():
     assert lib.dlm_draft_step(None, 1, 1, 64, 64, 0, 16, 0.25, None, None, 0, None, None, None, None, None) == -1
     with pytest.raises(L.DlmError):
         L.check(-1, "x")
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py runs on one GPU: --gpus 2 exits with status 2 and says why,
+    before any GPU work."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
