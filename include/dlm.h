@@ -52,6 +52,9 @@ typedef enum {
  * RMSNorm and an untied LM head.  mask_id is the [MASK] token id.
  * Supported: head_dim 64 or 128; d_model, n_heads*head_dim multiples of 128;
  * ffn widths multiples of 64; n_experts <= 256; top_k <= 8; vocab >= 2.
+ * Shapes: batch * (prompt_len + draft_len) tokens times max(d_model,
+ * n_heads*head_dim) bf16 values must stay below 2 GiB (the kernels address
+ * activations with 32-bit offsets); larger shapes are DLM_ERR_INVALID_ARG.
  */
 typedef struct dlm_config {
     int32_t n_layers;
@@ -80,7 +83,21 @@ typedef struct dlm_stats {
     int32_t n_edited;       /* real-token slots that changed                     */
     int32_t n_masked_left;  /* [MASK] slots left at the end (dlm_refine only)    */
     int32_t steps_run;      /* passes executed (dlm_refine only)                 */
+    int32_t n_invalid;      /* token ids outside [0, vocab), or mask_id in the   */
+                            /* prompt, seen by the pass (it then wrote nothing)  */
 } dlm_stats;
+
+/*
+ * Token validation (Sec. 4.2: the prompt is fixed context, only the draft is
+ * editable, so the prompt holds real tokens).  Every pass checks on the device
+ * that each token id lies in [0, vocab) and that no prompt slot holds mask_id.
+ * A pass that finds such an id updates no slot and counts the ids in
+ * dlm_stats.n_invalid.  The entry points that synchronise once per pass
+ * (dlm_refine, dlm_refine_ex, dlm_refine_local, dlm_draft, dlm_cascade) read
+ * the count at that synchronisation and return DLM_ERR_INVALID_ARG; the
+ * asynchronous single-pass entry points (dlm_refine_step*, dlm_draft_step)
+ * report it through d_stats only.
+ */
 
 /* Bytes of device memory the weights of cfg occupy (0 if cfg is invalid). */
 size_t dlm_weights_bytes(const dlm_config* cfg);
@@ -116,11 +133,12 @@ dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void
  * confidence conf = 1 / sum_v exp(z_v - max z), then all draft positions are
  * updated at once: a slot takes t* when t* != mask_id and conf >= threshold.
  * Prompt slots are never written.  Draft slots may hold mask_id; the prompt
- * may not (DLM_ERR_INVALID_ARG is not detectable on device: such a prompt is
- * processed as an ordinary token).
+ * may not (see token validation above: such a pass writes nothing and
+ * d_stats->n_invalid counts the offending ids).
  * Optional outputs (NULL to skip), device pointers:
  *   d_top1 int32 [batch][draft_len], d_conf float [batch][draft_len],
- *   d_stats dlm_stats (n_unmasked, n_edited of this pass; other fields 0).
+ *   d_stats dlm_stats (n_unmasked, n_edited, n_invalid of this pass; other
+ *   fields 0).
  * threshold must not be NaN (any other float is accepted; > 1 edits nothing,
  * <= 0 takes every top-1 that is not mask_id).
  */
@@ -136,7 +154,8 @@ dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int3
  * is read only; d_draft int32 [batch][draft_len] is updated in place.  Blocks
  * the calling thread once per pass (a 16-byte device-to-host copy) to decide the
  * early stop.  h_stats (host, may be NULL) receives totals over all passes.
- * n_steps = 0 only applies the mask set.
+ * n_steps = 0 only applies the mask set.  A pass that finds an invalid token id
+ * ends the call with DLM_ERR_INVALID_ARG and d_draft unchanged.
  */
 dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                       const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask,
@@ -322,7 +341,9 @@ dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, in
  * dlm_debug_layer: one block `layer` applied to the float residual stream
  *   d_x_in [batch*seq][d_model], result to d_x_out (may equal d_x_in); for a
  *   mixture-of-experts layer d_route_ids (may be NULL) receives the selected
- *   experts int32 [batch*seq][top_k] in selection order.
+ *   experts int32 [batch*seq][top_k] in selection order and d_router_logits
+ *   (may be NULL) the router logits float [batch*seq][n_experts] they were
+ *   selected from.
  * dlm_debug_head: final norm + LM head + fused reduction on a float residual
  *   stream d_x [batch*(prompt_len+draft_len)][d_model] (draft rows used).
  */
@@ -332,7 +353,8 @@ dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, in
                              int32_t* d_top1, float* d_conf, float* d_logits);
 dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len,
                            const float* d_x_in, float* d_x_out, void* d_workspace,
-                           size_t workspace_bytes, void* hip_stream, int32_t* d_route_ids);
+                           size_t workspace_bytes, void* hip_stream, int32_t* d_route_ids,
+                           float* d_router_logits);
 dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                           const float* d_x, void* d_workspace, size_t workspace_bytes,
                           void* hip_stream, float* d_max_logit, int32_t* d_top1, float* d_conf);

@@ -77,7 +77,7 @@ def block_bounds(prompt_len: int, draft_len: int, block_len: int, k: int):
     return start, min(start + block_len, prompt_len + draft_len)
 
 
-def draft_forward_block(W, tokens: np.ndarray, prompt_len: int, block_len: int, k: int, decide_bf16: bool = True):
+def draft_forward_block(W, tokens: np.ndarray, prompt_len: int, block_len: int, k: int, decide_bf16: bool = False):
     """Forward over the prefix that ends with block k under the block-causal
     mask; top-1, confidence and logit statistics of block k's positions."""
     B, S = tokens.shape
@@ -90,7 +90,7 @@ def draft_forward_block(W, tokens: np.ndarray, prompt_len: int, block_len: int, 
 
 
 def draft_step(W, tokens: np.ndarray, prompt_len: int, block_len: int, k: int, tau: float, steps_left: int,
-               decide_bf16: bool = True):
+               decide_bf16: bool = False):
     """One denoising step on block k of tokens [B, S]: returns the new tokens
     and the step's info (top1, conf, margin of the block, sel, n_unmasked)."""
     start, end = block_bounds(prompt_len, tokens.shape[1] - prompt_len, block_len, k)
@@ -105,7 +105,7 @@ def draft_step(W, tokens: np.ndarray, prompt_len: int, block_len: int, k: int, t
 
 
 def draft(W, prompt: np.ndarray, draft_len: int, block_len: int, steps: int, tau: float,
-          decide_bf16: bool = True):
+          decide_bf16: bool = False):
     """Block-AR drafting of draft_len tokens after prompt [B, P].
 
     Returns (draft [B, draft_len], stats) with stats = {"steps_run": passes
@@ -132,7 +132,7 @@ def draft(W, prompt: np.ndarray, draft_len: int, block_len: int, steps: int, tau
 
 
 def cascade(W_draft, W_refine, prompt: np.ndarray, draft_len: int, block_len: int, steps: int, tau_draft: float,
-            n_refine: int, tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = True):
+            n_refine: int, tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = False):
     """Draft with W_draft, then refine_ex with W_refine on the finished draft
     (no mask set).  Returns (refined draft, {"draft", "refine", "passes"})."""
     d, ds = draft(W_draft, prompt, draft_len, block_len, steps, tau_draft, decide_bf16)

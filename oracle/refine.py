@@ -31,11 +31,15 @@ All arithmetic is float64 on weights that hold bfloat16 values; there is no
 blocking, fusion or reordering beyond the matrix products themselves.
 
 Integer decisions taken from floating-point values -- which experts a token is
-routed to, and the top-1 token of each draft position -- are taken in the
-precision of the GPU kernels that take them: the router and the LM head read
-their input activations rounded to bfloat16 (the GEMM operand precision), and
-their logits follow exactly from those operands.  Pass decide_bf16=False for
-the fully exact variant.
+routed to, and the top-1 token of each draft position -- are taken from the
+exact float64 logits.  A bf16-rounded GPU path can decide differently only
+where those logits nearly tie; the parity tests exempt such positions by the
+tolerances of the method's contract (top-1/top-2 margin and distance from the
+threshold, router top-k gap) and check each exemption against the measured
+logit error.  decide_bf16=True is a diagnostic only: the router and the LM
+head then read their input activations rounded to bfloat16 first (the GEMM
+operand precision of the kernels), which shows how many exempt decisions the
+operand rounding alone explains.
 """
 
 from __future__ import annotations
@@ -119,12 +123,13 @@ def swiglu(h: np.ndarray, w_gate, w_up, w_down) -> np.ndarray:
     return (silu(g) * u) @ w_down.astype(F64).T
 
 
-def route(h: np.ndarray, w_router, k: int, decide_bf16: bool = True):
+def route(h: np.ndarray, w_router, k: int, decide_bf16: bool = False, return_logits: bool = False):
     """Softmax router, top-k (ties go to the lower expert id), renormalised.
 
     Returns ids [T, k], weights [T, k] and the logit gap between the k-th and
-    (k+1)-th ranked experts (inf when k == E).  With decide_bf16 the router
-    reads h rounded to bfloat16.
+    (k+1)-th ranked experts (inf when k == E), and with return_logits also the
+    router logits z [T, E].  With decide_bf16 (a diagnostic) the router reads h
+    rounded to bfloat16.
     """
     if decide_bf16:
         h = bf16_round(h)
@@ -140,13 +145,15 @@ def route(h: np.ndarray, w_router, k: int, decide_bf16: bool = True):
         gap = zs[:, 0] - zs[:, 1]
     else:
         gap = np.full(z.shape[0], np.inf)
+    if return_logits:
+        return ids, w, gap, z
     return ids, w, gap
 
 
-def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = True):
+def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = False):
     """Sum over the selected experts of w_j * SwiGLU_j(h), plus the shared experts."""
     T = h.shape[0]
-    ids, w, gap = route(h, L["w_router"], k, decide_bf16)
+    ids, w, gap, z = route(h, L["w_router"], k, decide_bf16, return_logits=True)
     out = np.zeros_like(h)
     for e in range(len(L["experts"])):
         rows, slot = np.nonzero(ids == e)
@@ -157,12 +164,12 @@ def moe_ffn(h: np.ndarray, L: dict, k: int, decide_bf16: bool = True):
         out[rows] += w[rows, slot][:, None] * y
     for (wg, wu, wd) in L["shared"]:
         out += swiglu(h, wg, wu, wd)
-    return out, ids, gap
+    return out, ids, gap, z
 
 
 # ---------------------------------------------------------------- forward
 
-def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, positions: np.ndarray | None = None,
+def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = False, positions: np.ndarray | None = None,
                   key_limit: np.ndarray | None = None):
     """One pre-norm block over x [B, S, d] (all positions; no attention mask
     unless key_limit [S] is given, see attention); positions [S] (default
@@ -171,7 +178,7 @@ def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, posit
     H, KV, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
     pos = np.arange(S) if positions is None else np.asarray(positions)
     x = x.astype(F64, copy=True)
-    info = {"route_gap": None, "route_ids": None}
+    info = {"route_gap": None, "route_ids": None, "router_logits": None}
     attn = np.empty((B, S, H * hd), dtype=F64)
     for b in range(B):
         h = rms_norm(x[b], L["g1"], shape.norm_eps)
@@ -186,14 +193,15 @@ def layer_forward(shape, L: dict, x: np.ndarray, decide_bf16: bool = True, posit
     if shape.n_experts == 0:
         ffn = swiglu(h2, L["w_gate"], L["w_up"], L["w_down"])
     else:
-        ffn, ids, gap = moe_ffn(h2, L, shape.top_k, decide_bf16)
+        ffn, ids, gap, z = moe_ffn(h2, L, shape.top_k, decide_bf16)
         info["route_gap"] = gap.reshape(B, S)
         info["route_ids"] = ids.reshape(B, S, -1)
+        info["router_logits"] = z.reshape(B, S, -1)
     x += ffn.reshape(B, S, d)
     return x, info
 
 
-def layer_forward_rows(shape, L: dict, x_seq: np.ndarray, rows: np.ndarray, decide_bf16: bool = True):
+def layer_forward_rows(shape, L: dict, x_seq: np.ndarray, rows: np.ndarray, decide_bf16: bool = False):
     """The block of layer_forward for one sequence x_seq [S, d], evaluated only
     at the positions `rows`: keys and values come from all S positions, the
     queries and everything after attention (which is per position) from the
@@ -210,17 +218,17 @@ def layer_forward_rows(shape, L: dict, x_seq: np.ndarray, rows: np.ndarray, deci
     kk = rope(kk, np.arange(S), shape.rope_theta)
     x = x_seq[rows] + attention(q, kk, v).reshape(len(rows), H * hd) @ L["wo"].astype(F64).T
     h2 = rms_norm(x, L["g2"], shape.norm_eps)
-    info = {"route_gap": None, "route_ids": None}
+    info = {"route_gap": None, "route_ids": None, "router_logits": None}
     if shape.n_experts == 0:
         x = x + swiglu(h2, L["w_gate"], L["w_up"], L["w_down"])
     else:
-        ffn, ids, gap = moe_ffn(h2, L, shape.top_k, decide_bf16)
+        ffn, ids, gap, z = moe_ffn(h2, L, shape.top_k, decide_bf16)
         x = x + ffn
-        info["route_gap"], info["route_ids"] = gap, ids
+        info["route_gap"], info["route_ids"], info["router_logits"] = gap, ids, z
     return x, info
 
 
-def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = True,
+def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = False,
             positions: np.ndarray | None = None, key_limit: np.ndarray | None = None):
     """Residual stream after the last layer (before the final norm): [B, S, d].
 
@@ -243,7 +251,7 @@ def forward(W, tokens: np.ndarray, collect: bool = False, decide_bf16: bool = Tr
 # ---------------------------------------------------------------- reduction
 
 def lm_head_reduce(W, x_rows: np.ndarray, row_chunk: int = 256, want_logits: bool = False,
-                   decide_bf16: bool = True):
+                   decide_bf16: bool = False):
     """Per row: logits z = (rms(x) g_f) Wlm^T over the full vocabulary (the
     normalised row rounded to bfloat16 when decide_bf16), then
 
@@ -309,7 +317,7 @@ def _reduce_draft(W, tokens: np.ndarray, prompt_len: int, decide_bf16: bool, pos
             "max_logit": red["max_logit"].reshape(B, D), "margin": red["margin"].reshape(B, D)}
 
 
-def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float, decide_bf16: bool = True):
+def refine_step(W, tokens: np.ndarray, prompt_len: int, tau: float, decide_bf16: bool = False):
     """One refinement pass over tokens [B, S] (prompt in [0, P), draft in [P, S))."""
     info = _reduce_draft(W, tokens, prompt_len, decide_bf16)
     new_draft, n_unm, n_edit = edit_rule(tokens[:, prompt_len:], info["top1"], info["conf"], tau, W.shape.mask_id)
@@ -341,7 +349,7 @@ def edit_rule_ex(draft: np.ndarray, top1: np.ndarray, conf: np.ndarray, tau_unma
 
 
 def refine_step_ex(W, tokens: np.ndarray, prompt_len: int, tau_unmask: float, tau_edit: float, eos_id: int = -1,
-                   decide_bf16: bool = True, span_start: int = 0):
+                   decide_bf16: bool = False, span_start: int = 0):
     """One refinement pass under edit_rule_ex.  With span_start, the draft part
     of tokens is a span of a longer draft: its token i sits at position
     prompt_len + span_start + i."""
@@ -359,7 +367,7 @@ def refine_step_ex(W, tokens: np.ndarray, prompt_len: int, tau_unmask: float, ta
 
 
 def refine_ex(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_steps: int,
-              tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = True):
+              tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = False):
     """refine() under edit_rule_ex: stops after a pass that changed nothing
     (stop_reason 1) or, with eos_id >= 0, after a pass that wrote eos_id into a
     draft slot (stop_reason 2); 0 when the pass budget ran out."""
@@ -387,7 +395,7 @@ def refine_ex(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None,
 
 
 def refine_local(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, schedule,
-                 tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = True):
+                 tau_unmask: float, tau_edit: float, eos_id: int = -1, decide_bf16: bool = False):
     """Local / staged refinement (Sec. 6.3 and Table 10: refinement in 64-token
     chunks of the generated span; App. D.4: staged schedules of span sizes).
     Reading used here: for each stage (span, passes) of the schedule, the draft
@@ -436,7 +444,7 @@ def refine_local(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | No
 
 
 def refine(W, prompt: np.ndarray, draft: np.ndarray, mask: np.ndarray | None, n_steps: int,
-           tau: float, decide_bf16: bool = True):
+           tau: float, decide_bf16: bool = False):
     """Draft positions in the mask set start as [MASK]; then up to n_steps passes,
     stopping after a pass that changed nothing.  Returns (final draft, stats)."""
     shape = W.shape

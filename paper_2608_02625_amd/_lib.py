@@ -31,7 +31,8 @@ class DlmConfig(ctypes.Structure):
 
 class DlmStats(ctypes.Structure):
     _fields_ = [("n_unmasked", ctypes.c_int32), ("n_edited", ctypes.c_int32),
-                ("n_masked_left", ctypes.c_int32), ("steps_run", ctypes.c_int32)]
+                ("n_masked_left", ctypes.c_int32), ("steps_run", ctypes.c_int32),
+                ("n_invalid", ctypes.c_int32)]
 
     def as_dict(self):
         return {f: int(getattr(self, f)) for f, _ in self._fields_}
@@ -81,7 +82,7 @@ SIGNATURES = [
     ("dlm_cascade", _I, [_P, _P, _I, _I, _I, _P, _P, _I, _I, _F, _I, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
                          ctypes.POINTER(DlmCascadeStats)]),
     ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
-    ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P]),
+    ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),
     ("dlm_debug_gemm", _I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),
     ("dlm_weight_info", _I, [_P, _I, _I, _I, ctypes.POINTER(_P), ctypes.POINTER(_I)]),

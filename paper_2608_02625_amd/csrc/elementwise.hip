@@ -6,11 +6,17 @@
 namespace {
 
 // x[t][:] = E[tok[t]][:] (bf16 -> fp32); one workgroup per token.
-// Ids outside [0, V) are clamped into range so that no read leaves the table.
+// Ids outside [0, V) are clamped into range so that no read leaves the table,
+// and counted in *invalid together with [MASK] ids in the first mask_rows
+// positions of each row of S tokens (the prompt, which must hold real tokens).
 __global__ void embed_kernel(const int32_t* __restrict__ tok, const bf16_t* __restrict__ emb,
-                             float* __restrict__ x, int d, int V) {
+                             float* __restrict__ x, int d, int V, int S, int mask_rows, int mask_id,
+                             int32_t* __restrict__ invalid) {
     const int t = blockIdx.x;
-    const int id = min(max(tok[t], 0), V - 1);
+    const int raw = tok[t];
+    if (threadIdx.x == 0 && invalid && (raw < 0 || raw >= V || (t % S < mask_rows && raw == mask_id)))
+        atomicAdd(invalid, 1);
+    const int id = min(max(raw, 0), V - 1);
     const bf16_t* src = emb + (int64_t)id * d;
     float* dst = x + (int64_t)t * d;
     for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
@@ -95,6 +101,7 @@ __global__ void edit_kernel(int32_t* __restrict__ tokens, int S, int P, int D,
                             int32_t* __restrict__ out_top1, float* __restrict__ out_conf, int n) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
     int unm = 0, edt = 0, eos = 0;
+    const bool rejected = counters[CNT_INVALID] != 0;      // the pass saw invalid token ids
     if (r < n) {
         const int b = r / D, i = r - b * D;
         int32_t* slot = tokens + (int64_t)b * S + P + i;
@@ -102,7 +109,7 @@ __global__ void edit_kernel(int32_t* __restrict__ tokens, int S, int P, int D,
         const int32_t t = top1[r];
         const float c = conf[r];
         const float thr = cur == mask_id ? thr_unmask : thr_edit;
-        if (t != mask_id && c >= thr && t != cur) {
+        if (!rejected && t != mask_id && c >= thr && t != cur) {
             *slot = t;
             if (cur == mask_id) unm = 1; else edt = 1;
             eos = t == eos_id;
@@ -112,8 +119,8 @@ __global__ void edit_kernel(int32_t* __restrict__ tokens, int S, int P, int D,
     }
     const unsigned long long bu = __ballot(unm), be = __ballot(edt), bx = __ballot(eos);
     if ((threadIdx.x & 63) == 0) {
-        if (bu) atomicAdd(&counters[0], (int)__popcll(bu));
-        if (be) atomicAdd(&counters[1], (int)__popcll(be));
+        if (bu) atomicAdd(&counters[CNT_UNMASKED], (int)__popcll(bu));
+        if (be) atomicAdd(&counters[CNT_EDITED], (int)__popcll(be));
         if (bx && eos_count) atomicAdd(eos_count, (int)__popcll(bx));
     }
 }
@@ -177,13 +184,20 @@ __global__ void count_masks_kernel(const int32_t* __restrict__ tokens, int S, in
     if ((threadIdx.x & 63) == 0 && bm) atomicAdd(counter, (int)__popcll(bm));
 }
 
-// Block-AR drafting: tokens [B][S] = prompt ‖ all [MASK].
+// Block-AR drafting: tokens [B][S] = prompt ‖ all [MASK]; prompt ids outside
+// [0, V) or equal to the [MASK] id are counted as invalid.
 __global__ void draft_init_kernel(const int32_t* __restrict__ prompt, int32_t* __restrict__ tokens, int P, int S,
-                                  int mask_id, int n) {
+                                  int V, int mask_id, int32_t* __restrict__ counters, int n) {
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= n) return;
-    const int b = idx / S, s = idx - b * S;
-    tokens[idx] = s < P ? prompt[(int64_t)b * P + s] : mask_id;
+    int bad = 0;
+    if (idx < n) {
+        const int b = idx / S, s = idx - b * S;
+        const int32_t v = s < P ? prompt[(int64_t)b * P + s] : mask_id;
+        bad = s < P && (v < 0 || v >= V || v == mask_id);
+        tokens[idx] = v;
+    }
+    const unsigned long long bb = __ballot(bad);
+    if ((threadIdx.x & 63) == 0 && bb) atomicAdd(&counters[CNT_INVALID], (int)__popcll(bb));
 }
 
 // out [B][L] = tokens[b][c0 .. c0 + L) of a [B][S] sequence.
@@ -213,6 +227,7 @@ __global__ __launch_bounds__(256) void draft_select_kernel(int32_t* __restrict__
     __shared__ int ms[1024];
     __shared__ int n_mask, n_above, n_unm, n_left;
     const int b = blockIdx.x;
+    if (counters[CNT_INVALID] != 0) return;              // the step saw invalid token ids: no update
     int32_t* row = tokens + (int64_t)b * S + c0;
     if (threadIdx.x == 0) n_mask = n_above = n_unm = n_left = 0;
     __syncthreads();
@@ -267,9 +282,9 @@ __global__ void vt_pad_zero_kernel(bf16_t* vt, int64_t n, int S, int pad, int st
 
 }  // namespace
 
-void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
-                  hipStream_t st) {
-    hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, st, tokens, emb, x, d, V);
+void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V, int S, int mask_rows,
+                  int mask_id, int32_t* invalid, hipStream_t st) {
+    hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, st, tokens, emb, x, d, V, S, mask_rows, mask_id, invalid);
 }
 
 void launch_rmsnorm(const float* x, const bf16_t* g, bf16_t* h, int rows, int d, float eps,
@@ -333,9 +348,11 @@ void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int m
                        mask_id, counter, n);
 }
 
-void launch_draft_init(const int32_t* prompt, int32_t* tokens, int B, int P, int S, int mask_id, hipStream_t st) {
+void launch_draft_init(const int32_t* prompt, int32_t* tokens, int B, int P, int S, int V, int mask_id,
+                       int32_t* counters, hipStream_t st) {
     const int n = B * S;
-    hipLaunchKernelGGL(draft_init_kernel, dim3((n + 255) / 256), dim3(256), 0, st, prompt, tokens, P, S, mask_id, n);
+    hipLaunchKernelGGL(draft_init_kernel, dim3((n + 255) / 256), dim3(256), 0, st, prompt, tokens, P, S, V, mask_id,
+                       counters, n);
 }
 
 void launch_window_gather(const int32_t* tokens, int32_t* out, int B, int S, int c0, int L, hipStream_t st) {

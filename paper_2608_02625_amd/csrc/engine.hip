@@ -212,7 +212,7 @@ Workspace plan_workspace(const dlm_config& c, int B, int P, int D) {
     w.top1 = add(R * 4);
     w.conf = add(R * 4);
     w.maxlogit = add(R * 4);
-    w.counters = add(sizeof(dlm_stats) + 16);          // pass counters, then the EOS count
+    w.counters = add(CNT_WORDS * 4);                   // pass counters (PassCounter)
     w.tokens = add(T * 4);
     return w;
 }
@@ -223,6 +223,14 @@ std::string check_shape(int B, int P, int D) {
     if (D <= 0) return "draft_len must be > 0";
     const int64_t S = (int64_t)P + D;
     if (S > 65536 || (int64_t)B * S > (1 << 26)) return "batch * seq_len too large";
+    return "";
+}
+
+// The kernels address the [tokens][d_model] and [tokens][heads * head_dim]
+// activations through 32-bit buffer offsets: such a buffer must stay below 2 GiB.
+std::string check_offsets(const dlm_config& c, int64_t T) {
+    const int64_t width = std::max<int64_t>(c.d_model, (int64_t)c.n_heads * c.head_dim);
+    if (T * width * 2 >= ((int64_t)1 << 31)) return "batch * seq_len * d_model too large (2 GiB activation buffers)";
     return "";
 }
 
@@ -267,6 +275,7 @@ struct Ctx {
     const float2* rope_all = nullptr;   // RoPE table of all kv_seq positions
     bool kv_only = false;               // stop after the last layer's K/V (cache commit)
     int att_split = 0, att_keys_lo = 0;  // window rows below att_split see only att_keys_lo keys
+    float* dbg_router_logits = nullptr;  // test hook: router logits [T][E] of the layer run
     template <class Tp>
     Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
     const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
@@ -411,7 +420,8 @@ dlm_status run_layer(Ctx& x, int l) {
     bf16_t* y = x.at<bf16_t>(x.w.y);
     {
         prof_begin(x, "router_topk");
-        hipError_t e = launch_router_topk(h, x.wt(L.wr), x.T, d, E, kk, ids, wts, slot, wg_counts, x.st);
+        hipError_t e = launch_router_topk(h, x.wt(L.wr), x.T, d, E, kk, ids, wts, slot, wg_counts, x.st,
+                                          x.dbg_router_logits);
         prof_end(x, "router_topk");
         if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("router_topk: ") + hipGetErrorString(e));
         prof_begin(x, "dispatch");
@@ -457,7 +467,9 @@ dlm_status run_prologue(Ctx& x, const int32_t* tokens) {
     LAUNCH(x, "rope_table", launch_rope_table(x.at<float2>(x.w.rope), x.S, c.head_dim / 2, (double)c.rope_theta, x.P,
                                               x.pos_shift, x.st));
     LAUNCH(x, "vt_pad_zero", launch_vt_pad_zero(x.at<bf16_t>(x.w.v), (int64_t)x.B * c.n_kv_heads * c.head_dim, x.S, x.st));
-    if (tokens) LAUNCH(x, "embed", launch_embed(tokens, x.wt(x.m->plan.emb), x.at<float>(x.w.x), x.T, c.d_model, c.vocab, x.st));
+    if (tokens)
+        LAUNCH(x, "embed", launch_embed(tokens, x.wt(x.m->plan.emb), x.at<float>(x.w.x), x.T, c.d_model, c.vocab, x.S,
+                                        x.P, c.mask_id, x.at<int32_t>(x.w.counters) + CNT_INVALID, x.st));
     return DLM_OK;
 }
 
@@ -485,6 +497,7 @@ dlm_status run_head(Ctx& x, int32_t* top1, float* conf, float* maxlogit, float* 
 dlm_status check_common(dlm_model* m, int B, int P, int D, void* ws, size_t ws_bytes, Workspace* w) {
     if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
     std::string e = check_shape(B, P, D);
+    if (e.empty()) e = check_offsets(m->cfg, (int64_t)B * (P + D));
     if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
     *w = plan_workspace(m->cfg, B, P, D);
     if (!ws) return fail(DLM_ERR_INVALID_ARG, "workspace is NULL");
@@ -504,8 +517,8 @@ dlm_status step_impl(Ctx& x, int32_t* tokens, const dlm_edit_rule& rule, int32_t
                      dlm_stats* stats_out, int32_t* eos_out = nullptr) {
     const dlm_config& c = x.c;
     int32_t* counters = x.at<int32_t>(x.w.counters);
-    int32_t* eos = counters + 4;
-    LAUNCH(x, "zero", launch_zero_i32(counters, 5, x.st));
+    int32_t* eos = counters + CNT_EOS;
+    LAUNCH(x, "zero", launch_zero_i32(counters, CNT_WORDS, x.st));
     TRY(run_prologue(x, tokens));
     for (int l = 0; l < c.n_layers; ++l) TRY(run_layer(x, l));
     TRY(run_head(x, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf), x.at<float>(x.w.maxlogit), nullptr));
@@ -561,7 +574,8 @@ std::string check_draft_shape(int B, int P, int D, int blk) {
 
 dlm_status check_draft(dlm_model* m, int B, int P, int D, int blk, void* ws, size_t ws_bytes, DraftPlan* p) {
     if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
-    const std::string e = check_draft_shape(B, P, D, blk);
+    std::string e = check_draft_shape(B, P, D, blk);
+    if (e.empty()) e = check_offsets(m->cfg, (int64_t)B * (P + D));
     if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
     *p = plan_draft(m->cfg, B, P, D, blk);
     if (!ws) return fail(DLM_ERR_INVALID_ARG, "workspace is NULL");
@@ -610,7 +624,9 @@ struct Drafter {
         }
         int32_t* wtok = x.at<int32_t>(p.wtok);
         LAUNCH(x, "window_gather", launch_window_gather(tokens, wtok, B, S, c0, L, st));
-        LAUNCH(x, "embed", launch_embed(wtok, x.wt(m->plan.emb), x.at<float>(p.w.x), x.T, c.d_model, c.vocab, st));
+        // a window inside the prompt must hold no [MASK] id; every id must lie in [0, vocab)
+        LAUNCH(x, "embed", launch_embed(wtok, x.wt(m->plan.emb), x.at<float>(p.w.x), x.T, c.d_model, c.vocab, L,
+                                        c0 + L <= P ? L : 0, c.mask_id, counters() + CNT_INVALID, st));
         for (int l = 0; l < c.n_layers; ++l) TRY(run_layer(x, l));
         if (head) TRY(run_head(x, x.at<int32_t>(p.w.top1), x.at<float>(p.w.conf), x.at<float>(p.w.maxlogit), nullptr));
         HIP_TRY(hipGetLastError());
@@ -656,6 +672,11 @@ struct Drafter {
     }
 };
 
+dlm_status fail_invalid_tokens(int n) {
+    return fail(DLM_ERR_INVALID_ARG, std::to_string(n) + " token id(s) outside [0, vocab) or [MASK] id(s) in the "
+                                     "prompt; the pass wrote nothing");
+}
+
 dlm_status check_rule(const dlm_config& c, const dlm_edit_rule* rule) {
     if (!rule) return fail(DLM_ERR_INVALID_ARG, "rule is NULL");
     if (isnan(rule->unmask_threshold) || isnan(rule->edit_threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
@@ -676,6 +697,7 @@ size_t dlm_weights_bytes(const dlm_config* cfg) {
 
 size_t dlm_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len) {
     if (!validate(cfg).empty() || !check_shape(batch, prompt_len, draft_len).empty()) return 0;
+    if (!check_offsets(*cfg, (int64_t)batch * (prompt_len + draft_len)).empty()) return 0;
     return plan_workspace(*cfg, batch, prompt_len, draft_len).total;
 }
 
@@ -746,21 +768,22 @@ dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_
     int32_t* counters = x.at<int32_t>(w.counters);
     launch_apply_mask(d_prompt, d_draft, d_mask, tokens, batch, prompt_len, draft_len, m->cfg.mask_id, x.st);
     HIP_TRY(hipGetLastError());
-    dlm_stats tot{0, 0, 0, 0};
+    dlm_stats tot{0, 0, 0, 0, 0};
     int32_t reason = 0;
     for (int s = 0; s < n_steps; ++s) {
         TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
-        int32_t st[5] = {};                           // the pass counters and the EOS count
+        int32_t st[CNT_WORDS] = {};                   // the pass counters
         HIP_TRY(hipMemcpyAsync(st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
         HIP_TRY(hipStreamSynchronize(x.st));
-        tot.n_unmasked += st[0];
-        tot.n_edited += st[1];
+        if (st[CNT_INVALID]) return fail_invalid_tokens(st[CNT_INVALID]);
+        tot.n_unmasked += st[CNT_UNMASKED];
+        tot.n_edited += st[CNT_EDITED];
         tot.steps_run += 1;
-        if (st[0] + st[1] == 0) {
+        if (st[CNT_UNMASKED] + st[CNT_EDITED] == 0) {
             reason = 1;
             break;
         }
-        if (rule->eos_id >= 0 && st[4] > 0) {
+        if (rule->eos_id >= 0 && st[CNT_EOS] > 0) {
             reason = 2;
             break;
         }
@@ -808,7 +831,7 @@ dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int
     const int n = batch * draft_len;
     if (d_mask) launch_mask_draft(d_draft, d_mask, n, m->cfg.mask_id, st);
     HIP_TRY(hipGetLastError());
-    dlm_stats tot{0, 0, 0, 0};
+    dlm_stats tot{0, 0, 0, 0, 0};
     int32_t reason = 1;                                // every chunk stopped on its own (or nothing ran)
     bool eos_stop = false;
     for (int g = 0; g < n_stages && !eos_stop; ++g) {
@@ -826,17 +849,18 @@ dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int
             bool still = false;
             for (int p = 0; p < h_passes[g]; ++p) {
                 TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
-                int32_t c[5] = {};
+                int32_t c[CNT_WORDS] = {};
                 HIP_TRY(hipMemcpyAsync(c, counters, sizeof(c), hipMemcpyDeviceToHost, st));
                 HIP_TRY(hipStreamSynchronize(st));
-                tot.n_unmasked += c[0];
-                tot.n_edited += c[1];
+                if (c[CNT_INVALID]) return fail_invalid_tokens(c[CNT_INVALID]);
+                tot.n_unmasked += c[CNT_UNMASKED];
+                tot.n_edited += c[CNT_EDITED];
                 tot.steps_run += 1;
-                if (c[0] + c[1] == 0) {
+                if (c[CNT_UNMASKED] + c[CNT_EDITED] == 0) {
                     still = true;
                     break;
                 }
-                if (rule->eos_id >= 0 && c[4] > 0) {
+                if (rule->eos_id >= 0 && c[CNT_EOS] > 0) {
                     eos_stop = true;
                     break;
                 }
@@ -872,6 +896,7 @@ dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t d
 size_t dlm_draft_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len,
                                  int32_t block_len) {
     if (!validate(cfg).empty() || !check_draft_shape(batch, prompt_len, draft_len, block_len).empty()) return 0;
+    if (!check_offsets(*cfg, (int64_t)batch * (prompt_len + draft_len)).empty()) return 0;
     return plan_draft(*cfg, batch, prompt_len, draft_len, block_len).total;
 }
 
@@ -888,6 +913,7 @@ dlm_status dlm_draft_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32
     if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
     const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len,
                      prompt_len + draft_len, block_len};
+    launch_zero_i32(dr.counters(), CNT_WORDS, dr.st);
     TRY(dr.begin(d_tokens));
     for (int j = 0; j < block_index; ++j) TRY(dr.run(d_tokens, dr.block_start(j), block_len, false));
     TRY(dr.step(d_tokens, block_index, threshold, steps_left, d_top1, d_conf));
@@ -910,19 +936,21 @@ dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t dr
     const int S = prompt_len + draft_len;
     const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len, S, block_len};
     int32_t* tokens = reinterpret_cast<int32_t*>((char*)d_workspace + p.tokens);
-    launch_draft_init(d_prompt, tokens, batch, prompt_len, S, m->cfg.mask_id, dr.st);
+    launch_zero_i32(dr.counters(), CNT_WORDS, dr.st);
+    launch_draft_init(d_prompt, tokens, batch, prompt_len, S, m->cfg.vocab, m->cfg.mask_id, dr.counters(), dr.st);
     HIP_TRY(hipGetLastError());
     TRY(dr.begin(tokens));
     const int n_blocks = (draft_len + block_len - 1) / block_len;
-    dlm_stats tot{0, 0, 0, 0};
+    dlm_stats tot{0, 0, 0, 0, 0};
     for (int k = 0; k < n_blocks; ++k) {
         int used = 0;
         for (int t = 0; t < steps_per_block; ++t) {
             // the first step of a block also commits the previous block's K/V
             TRY(dr.step(tokens, k, threshold, steps_per_block - t, nullptr, nullptr, t == 0 && k > 0));
-            int32_t c[4] = {};
+            int32_t c[CNT_WORDS] = {};
             HIP_TRY(hipMemcpyAsync(c, dr.counters(), sizeof(c), hipMemcpyDeviceToHost, dr.st));
             HIP_TRY(hipStreamSynchronize(dr.st));
+            if (c[CNT_INVALID]) return fail_invalid_tokens(c[CNT_INVALID]);
             ++used;
             tot.n_unmasked += c[0];
             if (c[2] == 0) break;                     // no [MASK] left in the block
@@ -1003,12 +1031,13 @@ dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, in
 
 dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len, const float* d_x_in,
                            float* d_x_out, void* d_workspace, size_t workspace_bytes, void* hip_stream,
-                           int32_t* d_route_ids) {
+                           int32_t* d_route_ids, float* d_router_logits) {
     Workspace w;
     TRY(check_common(m, batch, 0, seq_len, d_workspace, workspace_bytes, &w));
     if (layer < 0 || layer >= m->cfg.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
     if (!d_x_in || !d_x_out) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
     Ctx x = ctx_for(m, batch, 0, seq_len, d_workspace, w, hip_stream);
+    if (m->cfg.n_experts > 0) x.dbg_router_logits = d_router_logits;
     const size_t bytes = (size_t)x.T * m->cfg.d_model * 4;
     HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x_in, bytes, hipMemcpyDeviceToDevice, x.st));
     TRY(run_prologue(x, nullptr));

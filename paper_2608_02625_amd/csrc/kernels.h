@@ -79,9 +79,24 @@ hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* v, b
                             int Sq, int Skv, int n_keys, int H, int KV, int hd, hipStream_t st, int q_split = 0,
                             int n_keys_lo = 0);
 
+// Per-pass counters in the workspace (int32 words; the first five are the
+// dlm_stats layout).
+enum PassCounter {
+    CNT_UNMASKED = 0,     // [MASK] slots that took a token
+    CNT_EDITED = 1,       // real-token slots that changed
+    CNT_MASKED_LEFT = 2,
+    CNT_STEPS = 3,
+    CNT_INVALID = 4,      // token ids outside [0, V), or [MASK] ids in the prompt
+    CNT_EOS = 5,          // slots newly set to the EOS id
+    CNT_WORDS = 6
+};
+
 // ----------------------------------------------------------------- elementwise.hip
-void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V,
-                  hipStream_t st);
+// x[t] = E[tokens[t]] for T = rows of S tokens.  Ids outside [0, V) are
+// clamped for the read and counted in *invalid, as are [MASK] ids among the
+// first mask_rows tokens of each row of S (the prompt).
+void launch_embed(const int32_t* tokens, const bf16_t* emb, float* x, int T, int d, int V, int S, int mask_rows,
+                  int mask_id, int32_t* invalid, hipStream_t st);
 void launch_rmsnorm(const float* x, const bf16_t* g, bf16_t* h, int rows, int d, float eps,
                     hipStream_t st);
 // rows (b, P + i) for i < D of a [B][S] stream -> h [B*D][d]
@@ -90,8 +105,9 @@ void launch_rmsnorm_draft_rows(const float* x, const bf16_t* g, bf16_t* h, int B
 void launch_lmhead_merge(const float4* partials, int n_tiles, int R, int32_t* top1, float* conf,
                          float* max_logit, hipStream_t st);
 // Threshold update of every draft slot ([MASK] slots against thr_unmask,
-// real tokens against thr_edit); counters[0] += unmasked, counters[1] +=
-// edited, *eos_count (if not null) += slots newly set to eos_id.
+// real tokens against thr_edit); counters[CNT_UNMASKED] += unmasked,
+// counters[CNT_EDITED] += edited, *eos_count (if not null) += slots newly set
+// to eos_id.  Nothing is written when counters[CNT_INVALID] is set.
 void launch_edit(int32_t* tokens, int B, int S, int P, int D, const int32_t* top1, const float* conf,
                  float thr_unmask, float thr_edit, int mask_id, int eos_id, int32_t* counters,
                  int32_t* eos_count, int32_t* out_top1, float* out_conf, hipStream_t st);
@@ -108,11 +124,14 @@ void launch_copy_draft_out(const int32_t* tokens, int32_t* draft, int B, int S, 
 void launch_count_masks(const int32_t* tokens, int B, int S, int P, int D, int mask_id,
                         int32_t* counter, hipStream_t st);
 void launch_zero_i32(int32_t* p, int n, hipStream_t st);
-// Block-AR drafting: tokens [B][S] = prompt ‖ [MASK] ...; out [B][L] =
+// Block-AR drafting: tokens [B][S] = prompt ‖ [MASK] ... (prompt ids outside
+// [0, V) or equal to mask_id counted in counters[CNT_INVALID]); out [B][L] =
 // tokens[:, c0 : c0 + L]; the unmasking of one step on the block at c0 of
 // length L <= 1024 (top1 / conf [B][L]; counters[0] += slots given a real
-// token, counters[2] += masked slots left, counters[3] = 1).
-void launch_draft_init(const int32_t* prompt, int32_t* tokens, int B, int P, int S, int mask_id, hipStream_t st);
+// token, counters[2] += masked slots left, counters[3] = 1; nothing is
+// written when counters[CNT_INVALID] is set).
+void launch_draft_init(const int32_t* prompt, int32_t* tokens, int B, int P, int S, int V, int mask_id,
+                       int32_t* counters, hipStream_t st);
 void launch_window_gather(const int32_t* tokens, int32_t* out, int B, int S, int c0, int L, hipStream_t st);
 hipError_t launch_draft_select(int32_t* tokens, int B, int S, int c0, int L, const int32_t* top1, const float* conf,
                                float tau, int steps_left, int mask_id, int32_t* counters, int32_t* out_top1,
@@ -125,9 +144,10 @@ void launch_vt_pad_zero(bf16_t* vt, int64_t rows, int S, hipStream_t st);
 // top-k (k <= 8; ties -> lower id) with renormalised weights.  Tokens are
 // handled 32 per router workgroup: pos[t][j] = rank of the selection among its
 // workgroup's selections of expert ids[t][j]; wg_counts[E][ceil(T/32)] = per
-// expert and workgroup selection counts.
+// expert and workgroup selection counts.  logits (may be null): the router
+// logits float [T][E] (test hook).
 hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, int E, int k, int32_t* ids,
-                              float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st);
+                              float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st, float* logits = nullptr);
 // Group row ranges (E routed + n_shared groups of T rows), tile table of the
 // grouped GEMM (tile height bm), slot[t][j] (from pos, in place) and
 // a_rows[row] = token.  wg_counts is turned into per-workgroup offsets.

@@ -34,7 +34,7 @@ template <int NB, int ROWB>
 __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restrict__ h, const bf16_t* __restrict__ Wr,
                                                          int T, int d, int E, int k, int32_t* __restrict__ ids,
                                                          float* __restrict__ wts, int32_t* __restrict__ pos,
-                                                         int32_t* __restrict__ wg_counts) {
+                                                         int32_t* __restrict__ wg_counts, float* __restrict__ logits) {
     constexpr int NW = 8;                            // waves
     static_assert(NB >= 1 && NB <= NW, "expert blocks");
     constexpr int KSPLIT = NW / NB;                  // waves sharing an expert block
@@ -132,6 +132,7 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
         float z = zs[0][tt][e];
 #pragma unroll
         for (int s = 1; s < KSPLIT; ++s) z += zs[s][tt][e];
+        if (logits && e < E && t0 + tt < T) logits[(int64_t)(t0 + tt) * E + e] = z;   // test hook
         z = (e < E && z == z) ? z + 0.f : -INFINITY;         // (+0.f: -0 and +0 compare equal)
         zs[0][tt][e] = z;
         const uint32_t u = __float_as_uint(z);
@@ -354,30 +355,31 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
 
 template <int NB>
 void launch_router_nb(int rowb, dim3 grid, hipStream_t st, const bf16_t* h, const bf16_t* Wr, int T, int d, int E,
-                      int k, int32_t* ids, float* w, int32_t* pos, int32_t* wg_counts) {
+                      int k, int32_t* ids, float* w, int32_t* pos, int32_t* wg_counts, float* logits) {
     if constexpr (NB <= 2) {
         if (rowb == 512) {
             hipLaunchKernelGGL((router_topk_kernel<NB, 512>), grid, dim3(512), 0, st, h, Wr, T, d, E, k, ids, w, pos,
-                               wg_counts);
+                               wg_counts, logits);
             return;
         }
     }
     if constexpr (NB <= 4) {
         if (rowb == 256) {
             hipLaunchKernelGGL((router_topk_kernel<NB, 256>), grid, dim3(512), 0, st, h, Wr, T, d, E, k, ids, w, pos,
-                               wg_counts);
+                               wg_counts, logits);
             return;
         }
     }
     hipLaunchKernelGGL((router_topk_kernel<NB, 128>), grid, dim3(512), 0, st, h, Wr, T, d, E, k, ids, w, pos,
-                       wg_counts);
+                       wg_counts, logits);
 }
 
 }  // namespace
 
 hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, int E, int k, int32_t* ids,
-                              float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st) {
+                              float* w, int32_t* pos, int32_t* wg_counts, hipStream_t st, float* logits) {
     if (E < 1 || E > 256 || k < 1 || k > 8 || k > E || d % 64 != 0 || T < 1) return hipErrorInvalidValue;
+    if ((int64_t)T * d * 2 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;   // 32-bit buffer offsets into h
     const dim3 grid((T + 31) / 32), block(512);
     // The widest K chunk (256, 128 or 64 columns: 512, 256 or 128-byte LDS
     // rows, so the fewest stage barriers) that divides d and whose three
@@ -385,13 +387,13 @@ hipError_t launch_router_topk(const bf16_t* h, const bf16_t* Wr, int T, int d, i
     const int nb = E <= 32 ? 1 : E <= 64 ? 2 : E <= 128 ? 4 : 8;
     const int rowb = nb <= 2 && d % 256 == 0 ? 512 : nb <= 4 && d % 128 == 0 ? 256 : 128;
     if (E <= 32)
-        launch_router_nb<1>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<1>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts, logits);
     else if (E <= 64)
-        launch_router_nb<2>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<2>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts, logits);
     else if (E <= 128)
-        launch_router_nb<4>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<4>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts, logits);
     else
-        launch_router_nb<8>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts);
+        launch_router_nb<8>(rowb, grid, st, h, Wr, T, d, E, k, ids, w, pos, wg_counts, logits);
     return hipGetLastError();
 }
 

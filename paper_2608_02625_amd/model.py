@@ -243,16 +243,23 @@ class Refiner:
             out["logits"] = lg
         return out
 
-    def debug_layer(self, layer: int, x: torch.Tensor, batch: int, seq_len: int, want_routes: bool = False):
+    def debug_layer(self, layer: int, x: torch.Tensor, batch: int, seq_len: int, want_routes: bool = False,
+                    want_router_logits: bool = False):
         """One block on the float residual stream x [batch*seq_len, d]; returns the new
-        stream, or (stream, expert ids [batch*seq_len, top_k]) with want_routes."""
+        stream, or (stream, expert ids [batch*seq_len, top_k]) with want_routes, or
+        (stream, ids, router logits [batch*seq_len, n_experts]) with want_router_logits."""
         ws = self.workspace(batch, 0, seq_len)
         y = torch.empty_like(x)
-        ids = None
-        if want_routes and self.cfg.n_experts > 0:
+        ids = z = None
+        if (want_routes or want_router_logits) and self.cfg.n_experts > 0:
             ids = torch.empty(batch * seq_len, self.cfg.top_k, dtype=torch.int32, device=self.device)
+        if want_router_logits and self.cfg.n_experts > 0:
+            z = torch.empty(batch * seq_len, self.cfg.n_experts, dtype=torch.float32, device=self.device)
         check(self.lib.dlm_debug_layer(self._handle, layer, batch, seq_len, x.data_ptr(), y.data_ptr(),
-                                       ws.data_ptr(), ws.numel(), self.stream, _ptr(ids)), "dlm_debug_layer")
+                                       ws.data_ptr(), ws.numel(), self.stream, _ptr(ids), _ptr(z)),
+              "dlm_debug_layer")
+        if want_router_logits:
+            return y, ids, z
         return (y, ids) if want_routes else y
 
     def debug_head(self, x: torch.Tensor, batch: int, prompt_len: int, draft_len: int):

@@ -75,6 +75,11 @@ def test_size_queries_and_validation():
     for bad in (dict(head_dim=96), dict(top_k=9), dict(mask_id=157184), dict(n_heads=15),
                 dict(expert_ffn_dim=100), dict(n_experts=300), dict(vocab=1)):
         assert lib.dlm_weights_bytes(ctypes.byref(_cfg(L, **bad))) == 0, bad
+    # Activations are addressed with 32-bit buffer offsets: a [tokens][d_model]
+    # bf16 buffer must stay below 2 GiB.  d 2048: 2^19 tokens are 2 GiB exactly.
+    assert lib.dlm_workspace_bytes(ctypes.byref(cfg), 512, 0, 1023) > 0        # 523776 tokens
+    assert lib.dlm_workspace_bytes(ctypes.byref(cfg), 512, 1, 1023) == 0       # 2^19 tokens
+    assert lib.dlm_draft_workspace_bytes(ctypes.byref(cfg), 512, 1, 1023, 64) == 0
 
 
 def test_errors_are_reported_without_gpu_work():

@@ -67,27 +67,29 @@ def test_weights_sampled_bit_exact_large(large):
 
 def test_layer0_sampled_rows_large(large):
     """Block 0 on the embedded workload tokens: GPU on the whole batch, the
-    oracle at 8 sampled positions of sequence 0 (routing as in the mini-scale
-    test: positions whose experts differ must be router near-ties)."""
+    oracle at 8 sampled positions of sequence 0; routing checked token by
+    token as in the mini-scale test, hidden states on the positions routed
+    alike."""
     import torch
     from oracle.refine import layer_forward_rows
+    from tests.test_gpu_mini import check_routing
     w, R, W, toks = large
     s = w.model
     B, S, d = w.batch, w.seq_len, s.d_model
     x_in = W.embed_rows(toks).astype(np.float32)                       # [B, S, d]
     xg = torch.tensor(x_in.reshape(B * S, d), device="cuda")
-    y, ids = R.debug_layer(0, xg, B, S, want_routes=True)
+    y, ids, z = R.debug_layer(0, xg, B, S, want_router_logits=True)
     rows = np.sort(np.random.default_rng(8).choice(S, size=8, replace=False))
     log(f"[{w.name} layer 0] oracle block at {len(rows)} positions of sequence 0")
     ref, info = layer_forward_rows(s, W.layer(0), x_in[0].astype(np.float64), rows)
     got = _np(y).reshape(B, S, d)[0, rows]
     gids = _np(ids).reshape(B, S, -1)[0, rows]
-    same = np.all(np.sort(gids, -1) == np.sort(info["route_ids"], -1), -1)
+    gz = _np(z).reshape(B, S, -1)[0, rows]
+    same = check_routing(gids, gz, info["route_ids"], info["router_logits"], info["route_gap"],
+                         f"{w.name} layer 0")
     err = max_abs_rel(got[same], ref[same]) if same.any() else 0.0
-    worst = float(info["route_gap"][~same].max()) if (~same).any() else 0.0
-    log(f"[{w.name} layer 0] max-abs-rel {err:.2e} on {int(same.sum())}/{len(rows)} positions routed alike; "
-        f"largest oracle gap among the others {worst:.2e}")
-    assert same.sum() >= len(rows) - 1 and err <= HIDDEN_TOL and worst <= 3 * MARGIN
+    log(f"[{w.name} layer 0] hidden max-abs-rel {err:.2e} on {int(same.sum())}/{len(rows)} positions routed alike")
+    assert same.any() and err <= HIDDEN_TOL
 
 
 def test_head_sampled_rows_large(large):
@@ -121,7 +123,7 @@ def test_step_properties_large(large):
     B, P, D = w.batch, w.prompt_len, w.draft_len
     t0 = torch.tensor(toks, device="cuda")
     g = t0.clone()
-    st = torch.zeros(4, dtype=torch.int32, device="cuda")
+    st = torch.zeros(5, dtype=torch.int32, device="cuda")
     R.refine_step(g, P, 1.5, stats=st)
     assert torch.equal(g, t0) and _np(st)[:2].tolist() == [0, 0]
     outs = []

@@ -77,15 +77,37 @@ def test_weights_sampled_bit_exact_mini(mini):
         assert np.array_equal(got, ref), (f, kind, e)
 
 
+def check_routing(gpu_ids, gpu_logits, ref_ids, ref_logits, ref_gap, tag):
+    """Router parity, token by token.
+
+    The GPU's router logits must agree with the oracle's within 2e-2
+    max-abs-relative; the GPU must select exactly the top-k of its own logits
+    (descending, ties to the lower id); and a token whose expert set differs
+    from the oracle's is accepted only if the oracle's k-th/(k+1)-th logit gap
+    is at most twice that token's measured logit error, the only way the two
+    rankings can differ.  Returns the mask of tokens routed alike."""
+    T, k = gpu_ids.shape
+    ez = max_abs_rel(gpu_logits, ref_logits)
+    own = np.argsort(-gpu_logits, axis=-1, kind="stable")[:, :k]
+    err_t = np.max(np.abs(gpu_logits.astype(np.float64) - ref_logits), axis=-1)
+    same = np.all(np.sort(gpu_ids, -1) == np.sort(ref_ids, -1), -1)
+    flips = ~same
+    bad = flips & (ref_gap > 2 * err_t)
+    log(f"[{tag}] router logits max-abs-rel {ez:.2e} (per-token error up to {err_t.max():.2e}); "
+        f"{int(flips.sum())}/{T} tokens routed differently, oracle gaps "
+        f"{np.sort(ref_gap[flips])[:6].round(5).tolist() if flips.any() else []} "
+        f"against twice their errors {np.sort(2 * err_t[flips])[:6].round(5).tolist() if flips.any() else []}")
+    assert ez <= HIDDEN_TOL, (tag, ez)
+    assert np.array_equal(own, gpu_ids), tag
+    assert not bad.any(), (tag, int(bad.sum()))
+    return same
+
+
 @pytest.mark.parametrize("layer", [0, 19])
 def test_layer_teacher_forced_mini(mini, layer):
-    """One GPU block on the oracle's input (the embedded workload tokens).
-
-    Hidden states are compared on every token whose selected experts agree
-    with the oracle's; tokens routed differently must be router near-ties: the
-    oracle's k-th/(k+1)-th logit gap <= 3e-2 (bf16 rounding upstream of the
-    router -- attention output, normalised input -- moves router logits by up
-    to ~1.5e-2 here), which keeps such tokens to a few percent."""
+    """One GPU block on the oracle's input (the embedded workload tokens):
+    routing checked token by token (check_routing), hidden states within 2e-2
+    on every token routed alike."""
     import torch
     from oracle.refine import layer_forward
     w, R, W, toks = mini
@@ -95,17 +117,14 @@ def test_layer_teacher_forced_mini(mini, layer):
     log(f"[mini layer {layer}] oracle block over {B * S} tokens")
     ref, info = layer_forward(s, W.layer(layer), x_in)
     xg = torch.tensor(x_in.reshape(B * S, d), dtype=torch.float32, device="cuda")
-    y, ids = R.debug_layer(layer, xg, B, S, want_routes=True)
+    y, ids, z = R.debug_layer(layer, xg, B, S, want_router_logits=True)
     got = _np(y).reshape(B, S, d)
-    same = np.all(np.sort(_np(ids), -1) == np.sort(info["route_ids"].reshape(B * S, -1), -1), -1).reshape(B, S)
-    gap = info["route_gap"]
+    same = check_routing(_np(ids), _np(z), info["route_ids"].reshape(B * S, -1),
+                         info["router_logits"].reshape(B * S, -1), info["route_gap"].reshape(-1),
+                         f"mini layer {layer}").reshape(B, S)
     err = max_abs_rel(got[same], ref[same])
-    flips = int((~same).sum())
-    worst_gap = float(gap[~same].max()) if flips else 0.0
-    log(f"[mini layer {layer}] max-abs-rel {err:.2e} on {int(same.sum())}/{same.size} tokens routed alike; "
-        f"{flips} routed differently, largest oracle gap among them {worst_gap:.2e}")
+    log(f"[mini layer {layer}] hidden max-abs-rel {err:.2e} on {int(same.sum())}/{same.size} tokens routed alike")
     assert err <= HIDDEN_TOL
-    assert flips <= 0.05 * same.size and worst_gap <= 3 * MARGIN
 
 
 def test_head_teacher_forced_mini(mini):
@@ -144,13 +163,13 @@ def test_step_properties_mini(mini):
     g = t0.clone()
     t1 = torch.empty(B * D, dtype=torch.int32, device="cuda")
     cf = torch.empty(B * D, dtype=torch.float32, device="cuda")
-    st = torch.zeros(4, dtype=torch.int32, device="cuda")
+    st = torch.zeros(5, dtype=torch.int32, device="cuda")
     R.refine_step(g, P, 1.5, top1=t1, conf=cf, stats=st)
     assert torch.equal(g, t0) and _np(st)[:2].tolist() == [0, 0]
     g2 = t0.clone()
     t1b = torch.empty_like(t1)
     cfb = torch.empty_like(cf)
-    st2 = torch.zeros(4, dtype=torch.int32, device="cuda")
+    st2 = torch.zeros(5, dtype=torch.int32, device="cuda")
     R.refine_step(g2, P, -1.0, top1=t1b, conf=cfb, stats=st2)
     assert torch.equal(t1, t1b) and torch.equal(cf, cfb)              # deterministic
     top = _np(t1b).reshape(B, D)

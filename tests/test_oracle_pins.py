@@ -232,11 +232,11 @@ def test_moe_expert_permutation_invariance():
     E, F, d = 6, 12, 10
     L = _moe_layer(rng, E, F, d, 1)
     h = rng.standard_normal((30, d))
-    out, _, _ = moe_ffn(h, L, 2)
+    out, _, _, _ = moe_ffn(h, L, 2)
     perm = rng.permutation(E)
     Lp = {"w_router": L["w_router"][perm], "experts": [L["experts"][i] for i in perm],
           "shared": L["shared"]}
-    outp, _, _ = moe_ffn(h, Lp, 2)
+    outp, _, _, _ = moe_ffn(h, Lp, 2)
     assert np.allclose(out, outp, rtol=1e-12, atol=1e-14)
 
 
@@ -245,16 +245,16 @@ def test_moe_reductions():
     d, F = 10, 12
     h = rng.standard_normal((25, d))
     one = _moe_layer(rng, 1, F, d, 0)                      # E = 1, k = 1: dense SwiGLU
-    out, _, _ = moe_ffn(h, one, 1)
+    out, _, _, _ = moe_ffn(h, one, 1)
     assert np.allclose(out, swiglu(h, *one["experts"][0]), rtol=1e-13)
     same = _moe_layer(rng, 5, F, d, 0)                     # identical experts: weights sum to 1
     same["experts"] = [same["experts"][0]] * 5
-    out, _, _ = moe_ffn(h, same, 3)
+    out, _, _, _ = moe_ffn(h, same, 3)
     assert np.allclose(out, swiglu(h, *same["experts"][0]), rtol=1e-12)
     sh = _moe_layer(rng, 4, F, d, 1)                       # shared expert is always added
     routed = dict(sh, shared=[])
-    a, _, _ = moe_ffn(h, sh, 2)
-    b, _, _ = moe_ffn(h, routed, 2)
+    a, _, _, _ = moe_ffn(h, sh, 2)
+    b, _, _, _ = moe_ffn(h, routed, 2)
     assert np.allclose(a - b, swiglu(h, *sh["shared"][0]), rtol=1e-12, atol=1e-13)
 
 
