@@ -148,6 +148,24 @@ dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int3
                            float* d_conf, dlm_stats* d_stats);
 
 /*
+ * dlm_refine_step for callers that cannot allocate device memory or pass a
+ * workspace (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same pass and the same results, with the workspace in
+ * a static device array of DLM_STATIC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends.  The call allocates nothing.
+ * Shapes whose workspace (dlm_workspace_bytes) exceeds the array return
+ * DLM_ERR_WORKSPACE with nothing launched.  The model's device (current when
+ * its weights were loaded) must be current.  Every call on one GPU uses the
+ * same array: calls that overlap on one GPU (other streams, other threads,
+ * other models) race and must be serialised by the caller.  Arguments and
+ * results as dlm_refine_step.
+ */
+#define DLM_STATIC_SCRATCH_BYTES (64u << 20)
+dlm_status dlm_refine_step_static(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                                  int32_t* d_tokens, float threshold, void* hip_stream, int32_t* d_top1,
+                                  float* d_conf, dlm_stats* d_stats);
+
+/*
  * Refine a draft: slots with d_mask[b][i] != 0 start as mask_id (d_mask may be
  * NULL = empty mask set), then up to n_steps passes of dlm_refine_step,
  * stopping after a pass that changed no slot.  d_prompt int32 [batch][prompt_len]

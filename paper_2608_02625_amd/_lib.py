@@ -14,6 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdlm.so")
 
 DLM_OK = 0
+STATIC_SCRATCH_BYTES = 64 << 20      # DLM_STATIC_SCRATCH_BYTES of include/dlm.h
 STATUS_NAMES = {0: "DLM_OK", -1: "DLM_ERR_INVALID_ARG", -3: "DLM_ERR_HIP", -4: "DLM_ERR_UNSUPPORTED",
                 -5: "DLM_ERR_WORKSPACE"}
 
@@ -66,6 +67,7 @@ SIGNATURES = [
     ("dlm_workspace_bytes", _SZ, [_CFG, _I, _I, _I]),
     ("dlm_load_synthetic_weights", _I, [_CFG, ctypes.c_uint64, _P, _SZ, _P, ctypes.POINTER(_P)]),
     ("dlm_refine_step", _I, [_P, _I, _I, _I, _P, _F, _P, _SZ, _P, _P, _P, _P]),
+    ("dlm_refine_step_static", _I, [_P, _I, _I, _I, _P, _F, _P, _P, _P, _P]),
     ("dlm_refine", _I, [_P, _I, _I, _I, _P, _P, _P, _I, _F, _P, _SZ, _P, ctypes.POINTER(DlmStats)]),
     ("dlm_refine_step_ex", _I, [_P, _I, _I, _I, _P, ctypes.POINTER(DlmEditRule), _P, _SZ, _P, _P, _P, _P, _P]),
     ("dlm_refine_ex", _I, [_P, _I, _I, _I, _P, _P, _P, _I, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,

@@ -16,6 +16,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -244,6 +245,8 @@ struct ProfRec {
 struct dlm_model {
     dlm_config cfg;
     uint64_t seed;
+    int device = 0;              // device current at set-up (holds the weights)
+    char* scratch = nullptr;     // that device's copy of the static scratch array
     char* base;
     size_t bytes;
     WeightPlan plan;
@@ -274,6 +277,7 @@ struct Ctx {
     size_t kc_layer = 0, vc_layer = 0;  // elements per layer
     const float2* rope_all = nullptr;   // RoPE table of all kv_seq positions
     bool kv_only = false;               // stop after the last layer's K/V (cache commit)
+    bool no_events = false;             // no profiling events (the entry point allocates nothing)
     int att_split = 0, att_keys_lo = 0;  // window rows below att_split see only att_keys_lo keys
     float* dbg_router_logits = nullptr;  // test hook: router logits [T][E] of the layer run
     template <class Tp>
@@ -284,7 +288,7 @@ struct Ctx {
 // Profiling: HIP events around launches of kernels whose name matches the filter.
 void prof_begin(Ctx& x, const char* name) {
     dlm_model* m = x.m;
-    if (!m->prof_on) return;
+    if (!m->prof_on || x.no_events) return;
     if (!(m->prof_filter == "*" || m->prof_filter == name)) return;
     if (m->prof_used == m->prof.size()) {
         ProfRec r{name, nullptr, nullptr};
@@ -297,7 +301,7 @@ void prof_begin(Ctx& x, const char* name) {
 }
 void prof_end(Ctx& x, const char* name) {
     dlm_model* m = x.m;
-    if (!m->prof_on) return;
+    if (!m->prof_on || x.no_events) return;
     if (!(m->prof_filter == "*" || m->prof_filter == name)) return;
     if (m->prof_used >= m->prof.size()) return;
     hipEventRecord(m->prof[m->prof_used].b, x.st);
@@ -686,6 +690,39 @@ dlm_status check_rule(const dlm_config& c, const dlm_edit_rule* rule) {
 
 }  // namespace
 
+// Workspace of dlm_refine_step_static: a device array of fixed size, one copy
+// per GPU for the life of the process.  Host code never passes its name to a
+// kernel or a copy (on the host it names a stand-in, not device memory); it
+// uses the per-device address that hipGetSymbolAddress returns.
+static __device__ __align__(256) char scratch[DLM_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of this process's scratch array on the current device, resolved
+// once per device.
+dlm_status scratch_on_current_device(char** out, int* dev_out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(DLM_ERR_UNSUPPORTED, "device index >= 64");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(DLM_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        g_scratch_ptr[dev] = static_cast<char*>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    *dev_out = dev;
+    return DLM_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* dlm_last_error(void) { return g_last_error.c_str(); }
@@ -712,6 +749,9 @@ dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void
     WeightPlan plan = plan_weights(*cfg);
     if (weights_bytes < plan.total)
         return fail(DLM_ERR_WORKSPACE, "weights buffer too small: need " + std::to_string(plan.total) + " bytes");
+    char* scratch_ptr = nullptr;
+    int dev = 0;
+    TRY(scratch_on_current_device(&scratch_ptr, &dev));     // set-up: once per device
     hipStream_t st = (hipStream_t)hip_stream;
     char* base = (char*)d_weights;
     for (const TensorInit& t : plan.inits) {
@@ -727,6 +767,8 @@ dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void
     dlm_model* m = new dlm_model();
     m->cfg = *cfg;
     m->seed = seed;
+    m->device = dev;
+    m->scratch = scratch_ptr;
     m->base = base;
     m->bytes = weights_bytes;
     m->plan = std::move(plan);
@@ -752,6 +794,33 @@ dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int3
     const dlm_edit_rule rule{threshold, threshold, -1};
     return dlm_refine_step_ex(m, batch, prompt_len, draft_len, d_tokens, &rule, d_workspace, workspace_bytes,
                               hip_stream, d_top1, d_conf, d_stats, nullptr);
+}
+
+dlm_status dlm_refine_step_static(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
+                                  int32_t* d_tokens, float threshold, void* hip_stream, int32_t* d_top1,
+                                  float* d_conf, dlm_stats* d_stats) {
+    if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+    std::string e = check_shape(batch, prompt_len, draft_len);
+    if (e.empty()) e = check_offsets(m->cfg, (int64_t)batch * (prompt_len + draft_len));
+    if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
+    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev != m->device || !m->scratch)
+        return fail(DLM_ERR_INVALID_ARG, "the model's device (current when its weights were loaded) must be current");
+    const Workspace w = plan_workspace(m->cfg, batch, prompt_len, draft_len);
+    if (w.total > (size_t)DLM_STATIC_SCRATCH_BYTES)
+        return fail(DLM_ERR_WORKSPACE, "this shape needs " + std::to_string(w.total) +
+                                           " bytes of workspace; the static scratch holds " +
+                                           std::to_string((size_t)DLM_STATIC_SCRATCH_BYTES));
+    // Every buffer the pass reads before writing it in the same pass (the
+    // counters, the V^T padding) is cleared by a kernel of the pass itself,
+    // so whatever an earlier call left in the scratch does not matter.
+    const dlm_edit_rule rule{threshold, threshold, -1};
+    Ctx x = ctx_for(m, batch, prompt_len, draft_len, m->scratch, w, hip_stream);
+    x.no_events = true;
+    return step_impl(x, d_tokens, rule, d_top1, d_conf, d_stats, nullptr);
 }
 
 dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,

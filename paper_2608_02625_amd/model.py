@@ -93,6 +93,18 @@ class Refiner:
                                        _ptr(stats)), "dlm_refine_step")
         return tokens
 
+    def refine_step_static(self, tokens: torch.Tensor, prompt_len: int, threshold: float,
+                           top1: torch.Tensor | None = None, conf: torch.Tensor | None = None,
+                           stats: torch.Tensor | None = None):
+        """refine_step with the library's static scratch instead of a workspace
+        (dlm_refine_step_static: the call allocates nothing)."""
+        B, S = tokens.shape
+        D = S - prompt_len
+        check(self.lib.dlm_refine_step_static(self._handle, B, prompt_len, D, tokens.data_ptr(), float(threshold),
+                                              self.stream, _ptr(top1), _ptr(conf), _ptr(stats)),
+              "dlm_refine_step_static")
+        return tokens
+
     def refine(self, prompt: torch.Tensor, draft: torch.Tensor, mask: torch.Tensor | None, n_steps: int,
                threshold: float):
         """Refine draft (int32 [B, D], in place) given prompt [B, P] and mask (uint8/bool [B, D])."""
