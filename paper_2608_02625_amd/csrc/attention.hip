@@ -15,8 +15,8 @@
 // block's end), the others all n_keys.
 //
 // One workgroup = 4 waves = 128 queries of one (batch, head); each wave owns 32
-// queries.  Per 64-key tile, K [64 keys][hd] and V^T [hd][64 keys] are copied
-// global -> LDS by buffer loads (two stages, XOR-swizzled 16-byte chunks).
+// queries.  Per tile of KEYS keys, K [KEYS][hd] and V^T [hd][KEYS] are copied
+// global -> LDS by buffer loads (NS stages, XOR-swizzled 16-byte chunks).
 // Scores are computed transposed, S^T = K Q^T, so that each lane owns one
 // query column: the online-softmax statistics stay lane-local (plus one
 // exchange with lane^32) and the probabilities feed the next MFMA straight
@@ -32,9 +32,10 @@
 
 namespace {
 
-template <int HD>
+template <int HD, int KEYS_>
 struct AttnCfg {
-    static constexpr int KEYS = 64;                     // keys per tile
+    static constexpr int KEYS = KEYS_;                  // keys per tile (32 or 64)
+    static constexpr int NC = KEYS / 32;                // 32-key chunks per tile
     static constexpr int K_CPR = HD / 8;                // 16-byte chunks per K row
     static constexpr int K_ROW = HD * 2;
     static constexpr int K_BYTES = KEYS * K_ROW;
@@ -49,20 +50,24 @@ struct AttnCfg {
 };
 
 // XOR key of the 16-byte chunks of an LDS row of CPR chunks; fragment reads of
-// 32 consecutive rows at one logical chunk then hit distinct banks.
+// 32 consecutive rows at one logical chunk then hit distinct banks (with
+// 4-chunk rows, four consecutive rows share a 256-byte bank line, so the key
+// takes the row bits above them).
 template <int CPR>
 __device__ __forceinline__ int chunk_key(int row) {
     if constexpr (CPR == 16) return row & 15;
-    else return (row & 7) ^ ((row >> 3) & 1);
+    else if constexpr (CPR == 8) return (row & 7) ^ ((row >> 3) & 1);
+    else return (row >> 2) & 3;
 }
 
-template <int HD>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
+template <int HD, int KEYS, int WPE, int NS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
                                                    const bf16_t* Vt, bf16_t* __restrict__ O, int Sq, int Skv,
                                                    int n_keys, int q_split, int n_keys_lo, int H, int KV,
                                                    float scale_log2, uint32_t k_bytes, uint32_t v_bytes) {
-    using C = AttnCfg<HD>;
-    __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
+    using C = AttnCfg<HD, KEYS>;
+    static_assert(NS >= 2, "at least two K/V stages");
+    __shared__ __attribute__((aligned(16))) char smem[NS * C::STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);   // scalar: wave-level branches stay branches
     const int g = lane >> 5, j = lane & 31;
@@ -139,19 +144,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int vkey = chunk_key<C::V_CPR>(j);
 
     const int nkt = (n_keys + C::KEYS - 1) / C::KEYS;
-    issue(0, 0);
+    // Tiles kt .. kt + NS - 2 are in flight at the top of tile kt; copies past
+    // the last tile repeat it into a stage that is never read, so that every
+    // wait below counts the same number of copies.
+#pragma unroll
+    for (int t = 0; t < NS - 1; ++t) issue(min(t, nkt - 1), t);
+    int stage = 0;
     for (int kt = 0; kt < nkt; ++kt) {
-        wait_all_memory();                          // this wave's copies of tile kt landed
-        __syncthreads();                            // everyone's; stage of tile kt-1 is free
-        if (kt + 1 < nkt) issue(kt + 1, (kt + 1) & 1);
-        const int sb = (kt & 1) * C::STAGE;
+        wait_vmcnt<(NS - 2) * (C::K_INSTR + C::V_INSTR)>();   // this wave's copies of tile kt landed
+        __syncthreads();                            // everyone's; the stage of tile kt-1 is free
+        issue(min(kt + NS - 1, nkt - 1), stage == 0 ? NS - 1 : stage - 1);
+        const int sb = stage * C::STAGE;
+        stage = stage + 1 == NS ? 0 : stage + 1;
         const int k0 = kt * C::KEYS;
 
-        // S^T for 64 keys (two 32-key chunks): lane holds query j, keys
+        // S^T for the tile's keys (32-key chunks): lane holds query j, keys
         // c*32 + 8*(e/4) + 4*g + e%4.
-        f32x16 st[2];
+        f32x16 st[C::NC];
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < C::NC; ++c) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) st[c][e] = 0.f;
 #pragma unroll
@@ -163,14 +174,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
         }
         if (k0 + C::KEYS > lim) {                   // keys past the lane's limit are not visible
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+            for (int c = 0; c < C::NC; ++c)
 #pragma unroll
                 for (int e = 0; e < 16; ++e)
                     if (k0 + c * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= lim) st[c][e] = -INFINITY;
         }
         float mt = -INFINITY;
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < C::NC; ++c)
 #pragma unroll
             for (int e = 0; e < 16; ++e) mt = fmaxf(mt, st[c][e]);
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
@@ -186,9 +197,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
         }
         const float nb = -m_run * scale_log2;
         float lt = 0.f;
-        bf16x8 pf[2][2];
+        bf16x8 pf[C::NC][2];
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < C::NC; ++c)
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
                 u32x4 w;
@@ -207,7 +218,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 #pragma unroll
         for (int n = 0; n < C::NB; ++n)
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+            for (int c = 0; c < C::NC; ++c)
 #pragma unroll
                 for (int s2 = 0; s2 < 2; ++s2) {
                     const int off = sb + vfrag + n * 32 * C::V_ROW + (((4 * c + 2 * s2 + g) ^ vkey) << 4);
@@ -216,6 +227,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
                 }
     }
 
+    wait_all_memory();                              // no copy may still land in LDS when the workgroup ends
     l_run += __shfl_xor(l_run, 32, 64);
     if (q < Sq) {
         const float inv = 1.f / l_run;
@@ -245,12 +257,14 @@ hipError_t launch_attention(const bf16_t* q, const bf16_t* k, const bf16_t* vt, 
     // byte sizes of the K buffer (with its one-tile tail) and of V^T
     const int64_t kb = ((int64_t)B * KV * Skv + 64) * hd * 2, vb = (int64_t)B * KV * hd * vt_stride(Skv) * 2;
     if (kb >= 0x7fffffff || vb >= 0x7fffffff) return hipErrorInvalidValue;   // 32-bit buffer offsets
+    // 32-key tiles in three stages: 161 VGPRs at head_dim 128, so three
+    // workgroups (12 waves) share a CU (48 KB of LDS each).
     if (hd == 128)
-        hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, q_split, n_keys_lo, H, KV,
-                           scale_log2, (uint32_t)kb, (uint32_t)vb);
+        hipLaunchKernelGGL((attn_kernel<128, 32, 3, 3>), grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, q_split,
+                           n_keys_lo, H, KV, scale_log2, (uint32_t)kb, (uint32_t)vb);
     else if (hd == 64)
-        hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, q_split, n_keys_lo, H, KV,
-                           scale_log2, (uint32_t)kb, (uint32_t)vb);
+        hipLaunchKernelGGL((attn_kernel<64, 32, 3, 3>), grid, dim3(256), 0, st, q, k, vt, o, Sq, Skv, n_keys, q_split,
+                           n_keys_lo, H, KV, scale_log2, (uint32_t)kb, (uint32_t)vb);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -146,6 +146,27 @@ __device__ __forceinline__ void lds_barrier() {
 #endif
 }
 
+// Row segment of a transposed 32x32 accumulator block, for wide stores.  In
+// the transposed layout lane (r, h) = (lane % 32, lane / 32) holds columns
+// 8q + 4h .. 8q + 4h + 3 (q = 0..3) of row r; p[q] holds them as two packed
+// bf16 pairs.  Exchanging q = 2, 3 of lanes 0-31 with q = 0, 1 of lanes 32-63
+// (v_permlane32_swap) leaves lane (r, h) with columns 16h .. 16h + 15 of row
+// r in the order p[0], p[2], p[1], p[3]: two 16-byte stores per lane, a
+// 32-byte run of each row per pair of store instructions.
+__device__ __forceinline__ void swap_halves16(uint32_t (&p)[4][2]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const auto a = __builtin_amdgcn_permlane32_swap(p[0][k], p[2][k], false, false);
+        const auto b = __builtin_amdgcn_permlane32_swap(p[1][k], p[3][k], false, false);
+        p[0][k] = a[0];
+        p[2][k] = a[1];
+        p[1][k] = b[0];
+        p[3][k] = b[1];
+    }
+#endif
+}
+
 __device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }

@@ -344,27 +344,50 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         const bool full_tile = m0 + BM <= rows && n0 + BN <= a.N;
 
         if constexpr (EPI == EPI_BF16 && TACC) {
-            // 4 consecutive columns of one row per lane: one 8-byte store.
+            // Rows of 32-column blocks: after swap_halves16 a lane holds 16
+            // consecutive columns of its row, stored as two 16-byte writes
+            // (whole 32-byte runs: fewer partially written cache lines than
+            // 8-byte stores, which the store path pays for per line).  The
+            // exchange is done by every lane of the wave; rows past the end
+            // only skip their stores.
+            const bool wide = (a.ldo & 7) == 0;
+            const int half = lane >> 5;
 #pragma unroll
             for (int i = 0; i < T::TM; ++i) {
                 const int r = trow + i * 32;
-                if (r >= rows) continue;
                 bf16_t* orow = reinterpret_cast<bf16_t*>(a.out) + (GROUPED ? (int64_t)row_base + r : r) * a.ldo;
 #pragma unroll
-                for (int j = 0; j < T::TN; ++j)
+                for (int j = 0; j < T::TN; ++j) {
+                    const int cb = n0 + wn * T::WN + j * 32;           // first column of the block
+                    if (wide && cb + 32 <= a.N) {
+                        uint32_t p[4][2];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int c = tcol + j * 32 + 8 * q;
-                        const float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                            acc[i][j][4 * q + 3]};
-                        if (vec && c + 3 < a.N) {
-                            *reinterpret_cast<u32x2*>(orow + c) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                        } else {
+                        for (int q = 0; q < 4; ++q) {
+                            p[q][0] = pack_bf16x2(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
+                            p[q][1] = pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                        }
+                        swap_halves16(p);
+                        if (r < rows) {
+                            bf16_t* dst = orow + cb + 16 * half;
+                            *reinterpret_cast<u32x4*>(dst) = u32x4{p[0][0], p[0][1], p[2][0], p[2][1]};
+                            *reinterpret_cast<u32x4*>(dst + 8) = u32x4{p[1][0], p[1][1], p[3][0], p[3][1]};
+                        }
+                    } else if (r < rows) {
 #pragma unroll
-                            for (int t = 0; t < 4; ++t)
-                                if (c + t < a.N) orow[c + t] = f32_to_bf16(v[t]);
+                        for (int q = 0; q < 4; ++q) {
+                            const int c = tcol + j * 32 + 8 * q;
+                            const float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                                acc[i][j][4 * q + 3]};
+                            if (vec && c + 3 < a.N) {
+                                *reinterpret_cast<u32x2*>(orow + c) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                            } else {
+#pragma unroll
+                                for (int t = 0; t < 4; ++t)
+                                    if (c + t < a.N) orow[c + t] = f32_to_bf16(v[t]);
+                            }
                         }
                     }
+                }
             }
         } else if constexpr (EPI == EPI_RESID) {
             // out[row][col] += acc: per 32-row block all 16 x TN loads are issued
@@ -426,17 +449,20 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                 }
         } else if constexpr (EPI == EPI_SWIGLU) {
             // Physical columns alternate 32 gate / 32 up: blocks (j, j+1) hold the
-            // gate and up values of the same 32 features; 4 consecutive features
-            // per lane leave as one 8-byte store.
+            // gate and up values of the same 32 features.  As for the bf16 rows,
+            // swap_halves16 gives each lane 16 consecutive features, stored as
+            // two 16-byte writes.
+            const bool wide = (a.ldo & 7) == 0;
+            const int half = lane >> 5;
 #pragma unroll
             for (int i = 0; i < T::TM; ++i) {
                 const int r = trow + i * 32;
-                if (r >= rows) continue;
                 bf16_t* orow = reinterpret_cast<bf16_t*>(a.out) + (GROUPED ? (int64_t)row_base + r : r) * a.ldo;
 #pragma unroll
                 for (int j = 0; j < T::TN; j += 2) {
                     const int c0 = n0 + wn * T::WN + j * 32;                // first gate column of the pair
                     if (c0 >= a.N) continue;
+                    uint32_t p[4][2];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         float hv[4];
@@ -445,12 +471,25 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                             const float gt = acc[i][j][4 * q + t], up = acc[i][j + 1][4 * q + t];
                             hv[t] = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
                         }
-                        const int f = (c0 >> 1) + 8 * q + 4 * (lane >> 5);
-                        if (vec)
-                            *reinterpret_cast<u32x2*>(orow + f) = u32x2{pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
-                        else {
+                        p[q][0] = pack_bf16x2(hv[0], hv[1]);
+                        p[q][1] = pack_bf16x2(hv[2], hv[3]);
+                    }
+                    if (wide) {
+                        swap_halves16(p);
+                        if (r < rows) {
+                            bf16_t* dst = orow + (c0 >> 1) + 16 * half;
+                            *reinterpret_cast<u32x4*>(dst) = u32x4{p[0][0], p[0][1], p[2][0], p[2][1]};
+                            *reinterpret_cast<u32x4*>(dst + 8) = u32x4{p[1][0], p[1][1], p[3][0], p[3][1]};
+                        }
+                    } else if (r < rows) {
 #pragma unroll
-                            for (int t = 0; t < 4; ++t) orow[f + t] = f32_to_bf16(hv[t]);
+                        for (int q = 0; q < 4; ++q) {
+                            const int f = (c0 >> 1) + 8 * q + 4 * half;
+#pragma unroll
+                            for (int t = 0; t < 2; ++t) {
+                                orow[f + 2 * t] = (bf16_t)(p[q][t] & 0xffff);
+                                orow[f + 2 * t + 1] = (bf16_t)(p[q][t] >> 16);
+                            }
                         }
                     }
                 }
