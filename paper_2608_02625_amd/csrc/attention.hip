@@ -229,18 +229,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
 
     wait_all_memory();                              // no copy may still land in LDS when the workgroup ends
     l_run += __shfl_xor(l_run, 32, 64);
-    if (q < Sq) {
-        const float inv = 1.f / l_run;
-        bf16_t* orow = O + ((int64_t)b * Sq + q) * ((int64_t)H * HD) + (int64_t)h * HD;
+    // O^T accumulators: lane (query j, g) holds features n*32 + 8t + 4g .. +3;
+    // after swap_halves16 it holds n*32 + 16g .. +15, stored as two 16-byte
+    // writes (every lane takes part in the exchange; only rows q < Sq store).
+    const float inv = 1.f / l_run;
+    bf16_t* orow = O + ((int64_t)b * Sq + min(q, Sq - 1)) * ((int64_t)H * HD) + (int64_t)h * HD;
 #pragma unroll
-        for (int n = 0; n < C::NB; ++n)
+    for (int n = 0; n < C::NB; ++n) {
+        uint32_t p[4][2];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int hd0 = n * 32 + 8 * t + 4 * g;
-                const uint32_t w0 = pack_bf16x2(oacc[n][4 * t] * inv, oacc[n][4 * t + 1] * inv);
-                const uint32_t w1 = pack_bf16x2(oacc[n][4 * t + 2] * inv, oacc[n][4 * t + 3] * inv);
-                *reinterpret_cast<u32x2*>(orow + hd0) = u32x2{w0, w1};
-            }
+        for (int t = 0; t < 4; ++t) {
+            p[t][0] = pack_bf16x2(oacc[n][4 * t] * inv, oacc[n][4 * t + 1] * inv);
+            p[t][1] = pack_bf16x2(oacc[n][4 * t + 2] * inv, oacc[n][4 * t + 3] * inv);
+        }
+        swap_halves16(p);
+        if (q < Sq) {
+            bf16_t* dst = orow + n * 32 + 16 * g;
+            *reinterpret_cast<u32x4*>(dst) = u32x4{p[0][0], p[0][1], p[2][0], p[2][1]};
+            *reinterpret_cast<u32x4*>(dst + 8) = u32x4{p[1][0], p[1][1], p[3][0], p[3][1]};
+        }
     }
 }
 

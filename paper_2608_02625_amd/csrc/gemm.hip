@@ -88,8 +88,9 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
     const bool rotate = wrow < Hq + Hk;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-        const int t = n0 + lcol0 + j * 32;                    // token
-        if (t >= a.N) continue;
+        const int t_raw = n0 + lcol0 + j * 32;                // token
+        const bool live = t_raw < a.N;
+        const int t = live ? t_raw : a.N - 1;                 // lanes past the end compute, then store nothing
         const int b = t / S, s = t - b * S;
         const int sk = s + a.pos0;                            // position in K / V^T and the RoPE table
         if (rotate) {
@@ -105,12 +106,16 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
                     cs[ih][q][0] = p[0];
                     cs[ih][q][1] = p[1];
                 }
+            // Per 32-feature block: the rotated features of this lane's token,
+            // packed, then exchanged between lane halves (swap_halves16) so
+            // that each lane writes 16 consecutive features as two 16-byte
+            // stores.
+            const int half = (lrow0 >> 2) & 1;                  // lane / 32
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i) {
+                uint32_t p[4][2];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int f0 = m0 + lrow0 + i * 32 + 8 * q;       // first of 4 consecutive features
-                    const int hi0 = f0 % HD;
                     const int ih = (i % SPH) % POFF;
                     const float4 c01 = cs[ih][q][0], c23 = cs[ih][q][1];
                     const float cz[4] = {c01.x, c01.z, c23.x, c23.z};
@@ -125,11 +130,20 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, const f32x16 (&a
                         for (int r = 0; r < 4; ++r)
                             v[r] = acc[i][j][4 * q + r] * cz[r] + acc[(i + TM - POFF) % TM][j][4 * q + r] * sn[r];
                     }
-                    bf16_t* dst = f0 < Hq ? a.q + (((int64_t)b * a.n_heads + f0 / HD) * S + s) * HD + hi0
-                                          : a.k + (((int64_t)b * a.n_kv + (f0 - Hq) / HD) * SK + sk) * HD + hi0;
-                    *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                    p[q][0] = pack_bf16x2(v[0], v[1]);
+                    p[q][1] = pack_bf16x2(v[2], v[3]);
                 }
-        } else {
+                swap_halves16(p);
+                if (live) {
+                    const int fb = m0 + (lrow0 & ~4) + i * 32 + 16 * half;   // first of this lane's 16 features
+                    const int hi0 = fb % HD;
+                    bf16_t* dst = fb < Hq ? a.q + (((int64_t)b * a.n_heads + fb / HD) * S + s) * HD + hi0
+                                          : a.k + (((int64_t)b * a.n_kv + (fb - Hq) / HD) * SK + sk) * HD + hi0;
+                    *reinterpret_cast<u32x4*>(dst) = u32x4{p[0][0], p[0][1], p[2][0], p[2][1]};
+                    *reinterpret_cast<u32x4*>(dst + 8) = u32x4{p[1][0], p[1][1], p[3][0], p[3][1]};
+                }
+            }
+        } else if (live) {
             // V^T: per accumulator 4 rows (features) of one key column
             const int vs = vt_stride(SK);
 #pragma unroll
