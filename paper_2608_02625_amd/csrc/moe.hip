@@ -141,35 +141,45 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
     }
     __syncthreads();
 
-    // Top-k per token, one wave per token at a time; lane owns experts
+    // Top-k per token, four tokens per wave; lane owns experts
     // lane + 64q.  p = softmax(z) over the E experts; expert e is selection
     // r = #{e' : key[e'] > key[e]} if r < k (the k largest logits, ties ->
     // lower id, in descending order); the selected probabilities are
     // renormalised to sum to one.
     constexpr int NQ = (EP + 63) / 64;
     constexpr int TPW = 32 / NW;                     // tokens per wave
+    // Ranks of all of the wave's tokens in one pass over the keys (their LDS
+    // broadcast reads overlap).
+    uint64_t kq[TPW][NQ];
+    int rank[TPW][NQ];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int e = lane + 64 * q;
+            kq[i][q] = e < EP ? keys[(wave * TPW + i) * EP + e] : 0;
+            rank[i][q] = 0;
+        }
+#pragma unroll 8
+    for (int e2 = 0; e2 < EP; e2 += 2) {
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            const uint64_t* kr = keys + (wave * TPW + i) * EP;
+            const uint64_t k0 = kr[e2], k1 = kr[e2 + 1];
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) rank[i][q] += (k0 > kq[i][q]) + (k1 > kq[i][q]);
+        }
+    }
     for (int i = 0; i < TPW; ++i) {
         const int tt = wave * TPW + i, t = t0 + tt;
         const float* z = zs[0][tt];
-        const uint64_t* kr = keys + tt * EP;
         float v[NQ];
-        uint64_t kq[NQ];
-        int rank[NQ];
         float vm = -INFINITY;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int e = lane + 64 * q;
             v[q] = e < E ? z[e] : -INFINITY;
-            kq[q] = e < EP ? kr[e] : 0;
-            rank[q] = 0;
             vm = fmaxf(vm, v[q]);
-        }
-        // keys are wave-uniform LDS broadcasts, two per 16-byte read
-#pragma unroll 4
-        for (int e2 = 0; e2 < EP; e2 += 2) {
-            const uint64_t k0 = kr[e2], k1 = kr[e2 + 1];
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) rank[q] += (k0 > kq[q]) + (k1 > kq[q]);
         }
         const float m = wave_max_dpp(vm);
         float p[NQ], own = 0.f;
@@ -182,14 +192,14 @@ __global__ __launch_bounds__(512) void router_topk_kernel(const bf16_t* __restri
         float psel = 0.f;
 #pragma unroll
         for (int q = 0; q < NQ; ++q)
-            if (rank[q] < k) psel += p[q] / sum;
+            if (rank[i][q] < k) psel += p[q] / sum;
         const float psum = wave_sum_dpp(psel);
         if (t < T) {
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int e = lane + 64 * q;
-                if (e < E && rank[q] < k) {
-                    const int64_t o = (int64_t)t * k + rank[q];
+                if (e < E && rank[i][q] < k) {
+                    const int64_t o = (int64_t)t * k + rank[i][q];
                     ids[o] = e;
                     wts[o] = p[q] / sum / psum;
                     pos[o] = atomicAdd(&lcnt[e], 1);
@@ -228,43 +238,58 @@ __device__ void wave_scan512(const int* in, int* out, int n) {
     if (lane == 63) out[n] = incl;
 }
 
-// Dispatch plan (one workgroup of 16 waves).  For every expert e, wave e % 16
-// turns the row wg_counts[e][.] into exclusive offsets over the router
-// workgroups (in place) and keeps the row total.  Groups are the E routed
-// experts followed by n_shared shared experts of T rows each; their sizes are
-// scanned into grp_off[0..G], and the tile table (group, m0) of the grouped
-// GEMM and its length are written.
+// Dispatch plan (one workgroup of 16 waves).  The per-workgroup counts of
+// each routed expert e, wg_counts[e][0 .. nwg), become exclusive offsets over
+// the router workgroups (in place) and their total the group size: 16 threads
+// share an expert row, each summing a contiguous segment (loads issued eight
+// at a time), then a 16-lane scan gives each segment its start.  Groups are
+// the E routed experts followed by n_shared shared experts of T rows each;
+// their sizes are scanned into grp_off[0..G], and the tile table (group, m0)
+// of the grouped GEMM and its length are written.
 __global__ __launch_bounds__(1024) void dispatch_plan_kernel(int T, int E, int n_shared, int nwg, int bm,
                                                              int32_t* __restrict__ wg_counts,
                                                              int32_t* __restrict__ grp_off, int2* __restrict__ tile_tab,
                                                              int32_t* __restrict__ n_tiles) {
     __shared__ int cnt[512], off[513], ntl[512], toff[513];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int G = E + n_shared;
-    for (int e = wave; e < E; e += 16) {
-        int32_t* col = wg_counts + (int64_t)e * nwg;
-        int carry = 0;
-        for (int w0 = 0; w0 < nwg; w0 += 256) {
-            int v[4];
+    const int wave = threadIdx.x >> 6, sub = threadIdx.x & 15, row = threadIdx.x >> 4;
+    const int seg = (nwg + 15) >> 4;
+    const int w0 = min(sub * seg, nwg), w1 = min(w0 + seg, nwg);
+    for (int e0 = 0; e0 < E; e0 += 64) {
+        const int e = e0 + row;
+        const bool live = e < E;
+        int32_t* col = wg_counts + (int64_t)(live ? e : 0) * nwg;
+        int s = 0;
+        if (live) {
+            for (int w = w0; w < w1; w += 8) {
+                int v[8];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int wi = w0 + 64 * q + lane;
-                v[q] = wi < nwg ? col[wi] : 0;
-            }
+                for (int u = 0; u < 8; ++u) v[u] = w + u < w1 ? col[w + u] : 0;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int wi = w0 + 64 * q + lane;
-                int incl = v[q];
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) {
-                    const int u = __shfl_up(incl, o, 64);
-                    if (lane >= o) incl += u;
-                }
-                if (wi < nwg) col[wi] = carry + incl - v[q];
-                carry += __shfl(incl, 63, 64);
+                for (int u = 0; u < 8; ++u) s += v[u];
             }
         }
-        if (lane == 0) cnt[e] = carry;
+        int incl = s;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+            const int u = __shfl_up(incl, o, 16);
+            if (sub >= o) incl += u;
+        }
+        if (live) {
+            int run = incl - s;
+            for (int w = w0; w < w1; w += 8) {
+                int v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v[u] = w + u < w1 ? col[w + u] : 0;
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (w + u < w1) {
+                        col[w + u] = run;
+                        run += v[u];
+                    }
+            }
+            if (sub == 15) cnt[e] = incl;
+        }
     }
     for (int gi = E + threadIdx.x; gi < G; gi += blockDim.x) cnt[gi] = T;
     __syncthreads();
