@@ -60,6 +60,16 @@ __device__ __forceinline__ int chunk_key(int row) {
     else return (row >> 2) & 3;
 }
 
+// max / sum of v and its value in lane ^ 32 (v_permlane32_swap: no LDS trip)
+__device__ __forceinline__ float xor32_max(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int HD, int KEYS, int WPE, int NS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_kernel(const bf16_t* __restrict__ Q, const bf16_t* K,
                                                    const bf16_t* Vt, bf16_t* __restrict__ O, int Sq, int Skv,
@@ -165,11 +175,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
         for (int c = 0; c < C::NC; ++c) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) st[c][e] = 0.f;
+            // K fragments in batches of four reads issued together, so that the
+            // accumulation chain waits for one LDS latency per batch.
 #pragma unroll
-            for (int ks = 0; ks < C::NKS; ++ks) {
-                const int off = sb + c * 32 * C::K_ROW + kfrag + (((2 * ks + g) ^ kkey) << 4);
-                const bf16x8 kf = *(lds_frag*)((lds_char*)lds + off);
-                st[c] = mfma32x32x16(kf, qf[ks], st[c]);
+            for (int k4 = 0; k4 < C::NKS; k4 += 4) {
+                bf16x8 kf[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    kf[u] = *(lds_frag*)((lds_char*)lds + sb + c * 32 * C::K_ROW + kfrag + (((2 * (k4 + u) + g) ^ kkey) << 4));
+                sched_fence();
+#pragma unroll
+                for (int u = 0; u < 4; ++u) st[c] = mfma32x32x16(kf[u], qf[k4 + u], st[c]);
             }
         }
         if (k0 + C::KEYS > lim) {                   // keys past the lane's limit are not visible
@@ -184,7 +200,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
         for (int c = 0; c < C::NC; ++c)
 #pragma unroll
             for (int e = 0; e < 16; ++e) mt = fmaxf(mt, st[c][e]);
-        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        mt = xor32_max(mt);
         if (__any((mt - m_run) * scale_log2 > 8.f)) {
             const float m_new = fmaxf(m_run, mt);
             const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2);
@@ -214,21 +230,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
             }
         l_run += lt;
 
-        // O^T += V^T P^T: one 16-byte V^T read per fragment
+        // O^T += V^T P^T: one 16-byte V^T read per fragment, read in batches
+        // of four (two 32-row blocks of O^T)
 #pragma unroll
-        for (int n = 0; n < C::NB; ++n)
+        for (int c = 0; c < C::NC; ++c)
 #pragma unroll
-            for (int c = 0; c < C::NC; ++c)
+            for (int n2 = 0; n2 < C::NB; n2 += 2) {
+                bf16x8 vf[2][2];
 #pragma unroll
-                for (int s2 = 0; s2 < 2; ++s2) {
-                    const int off = sb + vfrag + n * 32 * C::V_ROW + (((4 * c + 2 * s2 + g) ^ vkey) << 4);
-                    const bf16x8 vf = *(lds_frag*)((lds_char*)lds + off);
-                    oacc[n] = mfma32x32x16(vf, pf[c][s2], oacc[n]);
-                }
+                for (int n = 0; n < 2; ++n)
+#pragma unroll
+                    for (int s2 = 0; s2 < 2; ++s2)
+                        vf[n][s2] = *(lds_frag*)((lds_char*)lds + sb + vfrag + (n2 + n) * 32 * C::V_ROW +
+                                                 (((4 * c + 2 * s2 + g) ^ vkey) << 4));
+                sched_fence();
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+                    for (int n = 0; n < 2; ++n) oacc[n2 + n] = mfma32x32x16(vf[n][s2], pf[c][s2], oacc[n2 + n]);
+            }
     }
 
     wait_all_memory();                              // no copy may still land in LDS when the workgroup ends
-    l_run += __shfl_xor(l_run, 32, 64);
+    l_run = xor32_sum(l_run);
     // O^T accumulators: lane (query j, g) holds features n*32 + 8t + 4g .. +3;
     // after swap_halves16 it holds n*32 + 16g .. +15, stored as two 16-byte
     // writes (every lane takes part in the exchange; only rows q < Sq store).
