@@ -550,12 +550,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
                                 if (!CHK || v < rows) s += __builtin_amdgcn_exp2f(acc[i][j][e] * kLog2e - ml);
                             }
                     }
-                    SoftmaxPartial p{m, idx, s};
-                    SoftmaxPartial q;
-                    q.m = __shfl_xor(p.m, 32, 64);
-                    q.idx = __shfl_xor(p.idx, 32, 64);
-                    q.s = __shfl_xor(p.s, 32, 64);
-                    part[j] = (lane < 32) ? sp_merge(p, q) : sp_merge(q, p);
+                    // Merge with lane ^ 32 (the other half of the column's rows):
+                    // v_permlane32_swap hands each lane its partner's values with
+                    // no LDS round trip; lanes below 32 hold the lower rows.
+                    const auto xm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+                    const auto xi = __builtin_amdgcn_permlane32_swap((uint32_t)idx, (uint32_t)idx, false, false);
+                    const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+                    const SoftmaxPartial lo{__uint_as_float(xm[0]), (int)xi[0], __uint_as_float(xs[0])};
+                    const SoftmaxPartial hi{__uint_as_float(xm[1]), (int)xi[1], __uint_as_float(xs[1])};
+                    part[j] = sp_merge(lo, hi);
                 }
             };
             if (m0 + BM <= rows)
