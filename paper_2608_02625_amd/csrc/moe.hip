@@ -304,6 +304,83 @@ __global__ __launch_bounds__(1024) void dispatch_plan_kernel(int T, int E, int n
         for (int t = 0; t < ntl[gi]; ++t) tile_tab[toff[gi] + t] = make_int2(gi, t * bm);
 }
 
+// Fused dispatch for small count tables: one workgroup per router workgroup
+// w (its 32 tokens).  Each workgroup derives from the per-expert counts
+// wg_counts[E][nwg] what it needs itself: every group's size (all routed
+// experts, then n_shared shared experts of T rows) and, per expert, how many
+// of that expert's selections come from router workgroups before w (4
+// threads per expert row, each summing a contiguous segment).  Workgroup 0
+// also writes grp_off, the tile table and its length.  The selections of the
+// workgroup's tokens then get their rows as in dispatch_scatter_kernel.  No
+// workgroup waits for another; the redundant reads of the count table
+// (E * nwg ints per workgroup) are why this is used for small tables only.
+__global__ __launch_bounds__(256) void dispatch_fused_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                              int n_shared, int nwg, int bm,
+                                                              const int32_t* __restrict__ wg_counts,
+                                                              int32_t* __restrict__ grp_off,
+                                                              int2* __restrict__ tile_tab,
+                                                              int32_t* __restrict__ n_tiles,
+                                                              int32_t* __restrict__ slot, int32_t* __restrict__ a_rows) {
+    __shared__ int tot[512], before[512], off[513], ntl[512], toff[513];
+    const int w = blockIdx.x, G = E + n_shared;
+    const int wave = threadIdx.x >> 6, q = threadIdx.x & 3, er = threadIdx.x >> 2;
+    const int seg = (nwg + 3) >> 2;
+    const int w0 = min(q * seg, nwg), w1 = min(w0 + seg, nwg);
+    for (int e0 = 0; e0 < E; e0 += 64) {
+        const int e = e0 + er;
+        int s_all = 0, s_pre = 0;
+        if (e < E) {
+            const int32_t* col = wg_counts + (int64_t)e * nwg;
+            for (int v0 = w0; v0 < w1; v0 += 8) {
+                int c[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) c[u] = v0 + u < w1 ? col[v0 + u] : 0;
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    s_all += c[u];
+                    if (v0 + u < w) s_pre += c[u];
+                }
+            }
+        }
+        s_all += __shfl_xor(s_all, 1, 64);
+        s_all += __shfl_xor(s_all, 2, 64);
+        s_pre += __shfl_xor(s_pre, 1, 64);
+        s_pre += __shfl_xor(s_pre, 2, 64);
+        if (e < E && q == 0) {
+            tot[e] = s_all;
+            before[e] = s_pre;
+        }
+    }
+    for (int gi = E + threadIdx.x; gi < G; gi += blockDim.x) tot[gi] = T;
+    __syncthreads();
+    for (int gi = threadIdx.x; gi < G; gi += blockDim.x) ntl[gi] = (tot[gi] + bm - 1) / bm;
+    __syncthreads();
+    if (wave == 0) wave_scan512(tot, off, G);
+    else if (wave == 1) wave_scan512(ntl, toff, G);
+    __syncthreads();
+    if (w == 0) {
+        for (int gi = threadIdx.x; gi <= G; gi += blockDim.x) grp_off[gi] = off[gi];
+        if (threadIdx.x == 0) *n_tiles = toff[G];
+        for (int gi = threadIdx.x; gi < G; gi += blockDim.x)
+            for (int t = 0; t < ntl[gi]; ++t) tile_tab[toff[gi] + t] = make_int2(gi, t * bm);
+    }
+    const int t0 = w * 32;
+    for (int il = threadIdx.x; il < 32 * k; il += blockDim.x) {
+        const int t = t0 + il / k;
+        if (t < T) {
+            const int64_t i = (int64_t)t0 * k + il;
+            const int e = ids[i];
+            const int sr = off[e] + before[e] + slot[i];
+            slot[i] = sr;
+            a_rows[sr] = t;
+        }
+    }
+    for (int il = threadIdx.x; il < 32 * n_shared; il += blockDim.x) {
+        const int t = t0 + (il & 31), sh = il >> 5;
+        if (t < T) a_rows[off[E + sh] + t] = t;
+    }
+}
+
 // Thread i < T*k turns the rank pos[i] of selection i into its row
 // slot[i] = grp_off[e] + (offset of its router workgroup at e) + pos[i]
 // (in place) and sets a_rows[slot] = token; the rest fill the shared groups.
@@ -427,6 +504,11 @@ hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared
                            hipStream_t st) {
     if (E + n_shared > 512) return hipErrorInvalidValue;
     const int nwg = (T + 31) / 32;
+    if ((int64_t)E * nwg <= 16384) {
+        hipLaunchKernelGGL(dispatch_fused_kernel, dim3(nwg), dim3(256), 0, st, ids, T, k, E, n_shared, nwg, bm,
+                           wg_counts, grp_off, tile_tab, n_tiles, slot, a_rows);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(dispatch_plan_kernel, dim3(1), dim3(1024), 0, st, T, E, n_shared, nwg, bm, wg_counts,
                        grp_off, tile_tab, n_tiles);
     const int64_t n = (int64_t)T * k + (int64_t)n_shared * T;
