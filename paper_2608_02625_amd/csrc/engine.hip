@@ -280,6 +280,10 @@ struct Ctx {
     bool no_events = false;             // no profiling events (the entry point allocates nothing)
     int att_split = 0, att_keys_lo = 0;  // window rows below att_split see only att_keys_lo keys
     float* dbg_router_logits = nullptr;  // test hook: router logits [T][E] of the layer run
+    // Only the draft rows leave the last block (the head reads nothing else):
+    // its MoE FFN then runs on the B*D draft rows alone.  Their K / V for the
+    // block's attention come from the QKV projection of every row, as before.
+    bool draft_rows_last_ffn = false;
     template <class Tp>
     Tp* at(size_t off) const { return reinterpret_cast<Tp*>(ws + off); }
     const bf16_t* wt(size_t off) const { return reinterpret_cast<const bf16_t*>(m->base + off); }
@@ -397,7 +401,13 @@ dlm_status run_layer(Ctx& x, int l) {
         const int obn = a.variant != 0 ? 256 : x.T <= 1024 ? 64 : 128;
         TRY(gemm(x, "gemm_o", a, EPI_RESID, false, obm, obn, 0));
     }
-    LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g2), h, x.T, d, c.norm_eps, x.st));
+    // MoE FFN of the last block on the draft rows only (rows in [B][D] order)
+    const bool draft_ffn = x.draft_rows_last_ffn && l + 1 == c.n_layers && c.n_experts > 0 && x.P > 0;
+    const int Tf = draft_ffn ? x.R : x.T;
+    if (draft_ffn)
+        LAUNCH(x, "rmsnorm", launch_rmsnorm_draft_rows(xs, x.wt(L.g2), h, x.B, x.S, x.P, x.D, d, c.norm_eps, x.st));
+    else
+        LAUNCH(x, "rmsnorm", launch_rmsnorm(xs, x.wt(L.g2), h, x.T, d, c.norm_eps, x.st));
     if (c.n_experts == 0) {
         const int F = c.ffn_dim;
         bf16_t* hf = x.at<bf16_t>(x.w.hf);
@@ -424,12 +434,12 @@ dlm_status run_layer(Ctx& x, int l) {
     bf16_t* y = x.at<bf16_t>(x.w.y);
     {
         prof_begin(x, "router_topk");
-        hipError_t e = launch_router_topk(h, x.wt(L.wr), x.T, d, E, kk, ids, wts, slot, wg_counts, x.st,
+        hipError_t e = launch_router_topk(h, x.wt(L.wr), Tf, d, E, kk, ids, wts, slot, wg_counts, x.st,
                                           x.dbg_router_logits);
         prof_end(x, "router_topk");
         if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("router_topk: ") + hipGetErrorString(e));
         prof_begin(x, "dispatch");
-        e = launch_dispatch(ids, x.T, kk, E, NS, kExpertBM, wg_counts, grp_off, tile_tab, n_tiles, slot, a_rows,
+        e = launch_dispatch(ids, Tf, kk, E, NS, kExpertBM, wg_counts, grp_off, tile_tab, n_tiles, slot, a_rows,
                             x.st);
         prof_end(x, "dispatch");
         if (e != hipSuccess) return fail(DLM_ERR_HIP, std::string("dispatch: ") + hipGetErrorString(e));
@@ -460,8 +470,9 @@ dlm_status run_layer(Ctx& x, int l) {
     }
     // The combine also normalises each finished row for the next block.
     const bool fuse = l + 1 < c.n_layers;
-    LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, x.T, kk, E, NS, d,
-                                        fuse ? x.wt(x.m->plan.layers[l + 1].g1) : nullptr, h, c.norm_eps, x.st));
+    LAUNCH(x, "combine", launch_combine(xs, y, slot, wts, grp_off, Tf, kk, E, NS, d,
+                                        fuse ? x.wt(x.m->plan.layers[l + 1].g1) : nullptr, h, c.norm_eps, x.st,
+                                        draft_ffn ? x.S : 0, draft_ffn ? x.P : 0, draft_ffn ? x.D : 0));
     x.h_ready = fuse;
     return DLM_OK;
 }
@@ -524,6 +535,7 @@ dlm_status step_impl(Ctx& x, int32_t* tokens, const dlm_edit_rule& rule, int32_t
     int32_t* eos = counters + CNT_EOS;
     LAUNCH(x, "zero", launch_zero_i32(counters, CNT_WORDS, x.st));
     TRY(run_prologue(x, tokens));
+    x.draft_rows_last_ffn = true;
     for (int l = 0; l < c.n_layers; ++l) TRY(run_layer(x, l));
     TRY(run_head(x, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf), x.at<float>(x.w.maxlogit), nullptr));
     LAUNCH(x, "edit", launch_edit(tokens, x.B, x.S, x.P, x.D, x.at<int32_t>(x.w.top1), x.at<float>(x.w.conf),

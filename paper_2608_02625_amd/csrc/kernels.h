@@ -157,6 +157,9 @@ hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared
 // x[t] += sum_j w[t][j] * Y[slot[t][j]] + sum_s Y[shared rows]
 // With g_next != nullptr, also writes h_next = RMSNorm(x) * g_next (bf16) for
 // the next block (the combine holds each finished residual row).
+// With map_D > 0 the T tokens are the draft rows of a [B][map_S] stream:
+// token t adds into residual row (t / map_D) * map_S + map_P + t % map_D.
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
                     const int32_t* grp_off, int T, int k, int E, int n_shared, int d,
-                    const bf16_t* g_next, bf16_t* h_next, float eps, hipStream_t st);
+                    const bf16_t* g_next, bf16_t* h_next, float eps, hipStream_t st, int map_S = 0,
+                    int map_P = 0, int map_D = 0);

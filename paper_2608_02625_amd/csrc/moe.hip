@@ -410,8 +410,10 @@ template <int NR>
 __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__ Y,
                                const int32_t* __restrict__ slot, const float* __restrict__ w,
                                const int32_t* __restrict__ grp_off, int k, int E, int n_shared,
-                               int d, const bf16_t* __restrict__ g_next, bf16_t* __restrict__ h_next, float eps) {
+                               int d, const bf16_t* __restrict__ g_next, bf16_t* __restrict__ h_next, float eps,
+                               int map_S, int map_P, int map_D) {
     const int t = blockIdx.x;
+    const int64_t xrow = map_D > 0 ? (int64_t)(t / map_D) * map_S + map_P + t % map_D : t;
     int rows[NR];
     float wt[NR];
 #pragma unroll
@@ -424,7 +426,7 @@ __global__ void combine_kernel(float* __restrict__ x, const bf16_t* __restrict__
             wt[r] = 1.f;
         }
     }
-    float* xr = x + (int64_t)t * d;
+    float* xr = x + xrow * d;
     float ss = 0.f;
     for (int i = threadIdx.x * 8; i < d; i += blockDim.x * 8) {
         u32x4 y[NR];
@@ -519,12 +521,12 @@ hipError_t launch_dispatch(const int32_t* ids, int T, int k, int E, int n_shared
 
 void launch_combine(float* x, const bf16_t* Y, const int32_t* slot, const float* w,
                     const int32_t* grp_off, int T, int k, int E, int n_shared, int d, const bf16_t* g_next,
-                    bf16_t* h_next, float eps, hipStream_t st) {
+                    bf16_t* h_next, float eps, hipStream_t st, int map_S, int map_P, int map_D) {
     const int nr = k + std::min(n_shared, 9 - k);
 #define COMBINE_CASE(N)                                                                                    \
     case N:                                                                                                \
         hipLaunchKernelGGL(combine_kernel<N>, dim3(T), dim3(256), 0, st, x, Y, slot, w, grp_off, k, E, n_shared, d, \
-                           g_next, h_next, eps);                                                           \
+                           g_next, h_next, eps, map_S, map_P, map_D);                                      \
         break;
     switch (nr) {
         COMBINE_CASE(1)

@@ -189,3 +189,23 @@ def test_invalid_tokens_are_rejected():
     st = torch.zeros(5, dtype=torch.int32, device="cuda")
     R.draft_step(g, P, 8, 0, 2, 0.0, stats=st)
     assert _np(st)[4] == 1 and np.array_equal(_np(g), tok)
+
+
+def test_step_draft_rows_equal_full_forward_moe():
+    """The step's last-block MoE FFN on the draft rows alone gives the same
+    top-1 tokens and confidences, bit for bit, as the full forward, also with
+    a prompt that is not a multiple of the router's 32-token groups."""
+    import torch
+    R, _ = _models(MOE)
+    rng = np.random.default_rng(5)
+    B, P, D = 3, 37, 45
+    toks = draw_tokens(rng, (B, P + D), MOE.vocab, "uniform").astype(np.int32)
+    toks[:, P + 3::7] = MOE.mask_id
+    g = _cuda_i32(toks)
+    out = R.debug_forward(g, P)
+    t1 = torch.empty(B * D, dtype=torch.int32, device="cuda")
+    cf = torch.empty(B * D, dtype=torch.float32, device="cuda")
+    R.refine_step(g.clone(), P, 1.5, top1=t1, conf=cf)
+    torch.cuda.synchronize()
+    assert torch.equal(t1, out["top1"]) and torch.equal(cf, out["conf"])
+

@@ -182,3 +182,23 @@ def test_step_properties_mini(mini):
     log(f"[mini step] tau=-1: unmasked {n_unm}, edited {int(changed.sum()) - n_unm}; "
         f"conf range [{float(cf.min()):.2e}, {float(cf.max()):.2e}]")
     assert _np(st2)[:2].tolist() == [n_unm, int(changed.sum()) - n_unm]
+
+
+def test_step_draft_rows_equal_full_forward_mini(mini):
+    """The refinement step runs the last block's MoE FFN on the draft rows
+    only (the prompt rows' outputs of that block reach nothing).  Its top-1
+    tokens and confidences must equal, bit for bit, those of the full forward
+    (every row through every block), at the benchmark's full size."""
+    import torch
+    w, R, W, toks = mini
+    P, D, B = w.prompt_len, w.draft_len, w.batch
+    g = torch.tensor(toks, device="cuda")
+    out = R.debug_forward(g, P)
+    t1 = torch.empty(B * D, dtype=torch.int32, device="cuda")
+    cf = torch.empty(B * D, dtype=torch.float32, device="cuda")
+    R.refine_step(g.clone(), P, 1.5, top1=t1, conf=cf)
+    torch.cuda.synchronize()
+    n_t = int((t1 != out["top1"]).sum())
+    n_c = int((cf != out["conf"]).sum())
+    log(f"[mini draft rows] top1 differing {n_t}, conf differing {n_c} of {B * D}")
+    assert n_t == 0 and n_c == 0
