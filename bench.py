@@ -57,31 +57,44 @@ def recorded_traffic(kernel, workload):
 
 
 def step_flops(shape, B, P, D):
-    """Algorithmic FLOPs of one pass: active experts only, LM head on draft rows only."""
+    """Algorithmic FLOPs of one pass: active experts only, LM head on draft
+    rows only.  Only the draft rows leave the last block, so there the prompt
+    rows need nothing but their K and V projections (the library still
+    computes their Q, attention and O product, which is not counted)."""
     S = P + D
     T = B * S
+    R = B * D
     d, hd, H, KV = shape.d_model, shape.head_dim, shape.n_heads, shape.n_kv_heads
-    per_tok = d * (H + 2 * KV) * hd + H * hd * d
     if shape.n_experts:
-        per_tok += d * shape.n_experts + (shape.top_k + shape.n_shared_experts) * 3 * d * shape.expert_ffn_dim
+        ffn = d * shape.n_experts + (shape.top_k + shape.n_shared_experts) * 3 * d * shape.expert_ffn_dim
     else:
-        per_tok += 3 * d * shape.ffn_dim
-    body = 2 * T * per_tok * shape.n_layers
-    attn = 4 * T * S * H * hd * shape.n_layers
-    head = 2 * B * D * d * shape.vocab
-    return body + attn + head
+        ffn = 3 * d * shape.ffn_dim
+    per_tok = d * (H + 2 * KV) * hd + H * hd * d + ffn
+    body = 2 * T * per_tok * (shape.n_layers - 1) + 4 * T * S * H * hd * (shape.n_layers - 1)
+    last = 2 * T * d * 2 * KV * hd + 2 * R * (d * H * hd + H * hd * d + ffn) + 4 * R * S * H * hd
+    head = 2 * R * d * shape.vocab
+    return body + last + head
+
+
+def expert_rows_per_launch(shape, B, P, D):
+    """Mean rows of one expert-GEMM launch over a pass: every row of every
+    block, except the last block, whose FFN runs on the B*D draft rows only
+    (when there is a prompt)."""
+    T = B * (P + D)
+    kr = shape.top_k + shape.n_shared_experts
+    last = B * D if P > 0 else T
+    return (T * (shape.n_layers - 1) + last) * kr / shape.n_layers
 
 
 def kernel_flops(name, shape, B, P, D):
-    """Algorithmic FLOPs of one launch of a named GEMM kernel."""
+    """Algorithmic FLOPs of one launch of a named GEMM kernel (for the expert
+    GEMMs the mean over one pass's launches)."""
     T = B * (P + D)
     d = shape.d_model
     if name == "gemm_expert_gate_up":
-        rows = T * (shape.top_k + shape.n_shared_experts)
-        return 2 * rows * d * 2 * shape.expert_ffn_dim
+        return 2 * expert_rows_per_launch(shape, B, P, D) * d * 2 * shape.expert_ffn_dim
     if name == "gemm_expert_down":
-        rows = T * (shape.top_k + shape.n_shared_experts)
-        return 2 * rows * shape.expert_ffn_dim * d
+        return 2 * expert_rows_per_launch(shape, B, P, D) * shape.expert_ffn_dim * d
     if name == "gemm_lm_head":
         return 2 * B * D * d * shape.vocab
     if name == "gemm_qkv":
