@@ -355,7 +355,11 @@ dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, in
  *   fused reduction to d_max_logit / d_top1 / d_conf [batch*draft_len].
  *   When d_logits is not NULL it also writes full float logits of the draft
  *   rows [batch*draft_len][vocab] through the same LM-head GEMM (test-only:
- *   the refine path never materialises logits).
+ *   the refine path never materialises logits).  For a mixture-of-experts
+ *   model, d_route_ids (may be NULL) receives every block's selected experts
+ *   int32 [n_layers][batch*(prompt_len+draft_len)][top_k] in selection order
+ *   and d_router_logits (may be NULL) the router logits they were selected
+ *   from, float [n_layers][batch*(prompt_len+draft_len)][n_experts].
  * dlm_debug_layer: one block `layer` applied to the float residual stream
  *   d_x_in [batch*seq][d_model], result to d_x_out (may equal d_x_in); for a
  *   mixture-of-experts layer d_route_ids (may be NULL) receives the selected
@@ -368,7 +372,8 @@ dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, in
 dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                              const int32_t* d_tokens, void* d_workspace, size_t workspace_bytes,
                              void* hip_stream, float* d_hidden, float* d_max_logit,
-                             int32_t* d_top1, float* d_conf, float* d_logits);
+                             int32_t* d_top1, float* d_conf, float* d_logits, int32_t* d_route_ids,
+                             float* d_router_logits);
 dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len,
                            const float* d_x_in, float* d_x_out, void* d_workspace,
                            size_t workspace_bytes, void* hip_stream, int32_t* d_route_ids,

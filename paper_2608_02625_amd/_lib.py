@@ -83,7 +83,7 @@ SIGNATURES = [
     ("dlm_cascade_workspace_bytes", _SZ, [_CFG, _CFG, _I, _I, _I, _I]),
     ("dlm_cascade", _I, [_P, _P, _I, _I, _I, _P, _P, _I, _I, _F, _I, ctypes.POINTER(DlmEditRule), _P, _SZ, _P,
                          ctypes.POINTER(DlmCascadeStats)]),
-    ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P]),
+    ("dlm_debug_forward", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P, _P, _P, _P, _P]),
     ("dlm_debug_layer", _I, [_P, _I, _I, _I, _P, _P, _P, _SZ, _P, _P, _P]),
     ("dlm_debug_head", _I, [_P, _I, _I, _I, _P, _P, _SZ, _P, _P, _P, _P]),
     ("dlm_debug_gemm", _I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),

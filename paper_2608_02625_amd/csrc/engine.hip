@@ -1090,13 +1090,21 @@ dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, in
 dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                              const int32_t* d_tokens, void* d_workspace, size_t workspace_bytes,
                              void* hip_stream, float* d_hidden, float* d_max_logit, int32_t* d_top1,
-                             float* d_conf, float* d_logits) {
+                             float* d_conf, float* d_logits, int32_t* d_route_ids, float* d_router_logits) {
     Workspace w;
     TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
     if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
     Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
     TRY(run_prologue(x, d_tokens));
-    for (int l = 0; l < m->cfg.n_layers; ++l) TRY(run_layer(x, l));
+    const size_t route_words = (size_t)x.T * m->cfg.top_k;
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+        if (d_router_logits && m->cfg.n_experts > 0)
+            x.dbg_router_logits = d_router_logits + (size_t)l * x.T * m->cfg.n_experts;
+        TRY(run_layer(x, l));
+        if (d_route_ids && m->cfg.n_experts > 0)
+            HIP_TRY(hipMemcpyAsync(d_route_ids + l * route_words, x.at<int32_t>(w.ids), route_words * 4,
+                                   hipMemcpyDeviceToDevice, x.st));
+    }
     if (d_hidden)
         HIP_TRY(hipMemcpyAsync(d_hidden, x.at<float>(w.x), (size_t)x.T * m->cfg.d_model * 4,
                                hipMemcpyDeviceToDevice, x.st));

@@ -237,7 +237,8 @@ class Refiner:
                                       _ptr(top1), _ptr(conf), _ptr(max_logit), _ptr(stats)), "dlm_draft_step")
         return tokens
 
-    def debug_forward(self, tokens: torch.Tensor, prompt_len: int, want_logits: bool = False):
+    def debug_forward(self, tokens: torch.Tensor, prompt_len: int, want_logits: bool = False,
+                      want_routes: bool = False):
         B, S = tokens.shape
         D = S - prompt_len
         ws = self.workspace(B, prompt_len, D)
@@ -247,12 +248,18 @@ class Refiner:
         t1 = torch.empty(B * D, dtype=torch.int32, device=dev)
         cf = torch.empty(B * D, dtype=torch.float32, device=dev)
         lg = torch.empty(B * D, self.cfg.vocab, dtype=torch.float32, device=dev) if want_logits else None
+        moe = want_routes and self.cfg.n_experts > 0
+        rt = torch.empty(self.cfg.n_layers, B * S, self.cfg.top_k, dtype=torch.int32, device=dev) if moe else None
+        rz = torch.empty(self.cfg.n_layers, B * S, self.cfg.n_experts, dtype=torch.float32, device=dev) if moe else None
         check(self.lib.dlm_debug_forward(self._handle, B, prompt_len, D, tokens.data_ptr(), ws.data_ptr(),
                                          ws.numel(), self.stream, hidden.data_ptr(), mx.data_ptr(), t1.data_ptr(),
-                                         cf.data_ptr(), _ptr(lg)), "dlm_debug_forward")
+                                         cf.data_ptr(), _ptr(lg), _ptr(rt), _ptr(rz)), "dlm_debug_forward")
         out = {"hidden": hidden, "max_logit": mx, "top1": t1, "conf": cf}
         if want_logits:
             out["logits"] = lg
+        if moe:
+            out["routes"] = rt          # [n_layers, B*S, top_k] selected experts per block
+            out["router_logits"] = rz   # [n_layers, B*S, n_experts]
         return out
 
     def debug_layer(self, layer: int, x: torch.Tensor, batch: int, seq_len: int, want_routes: bool = False,

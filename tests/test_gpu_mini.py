@@ -202,3 +202,55 @@ def test_step_draft_rows_equal_full_forward_mini(mini):
     n_c = int((cf != out["conf"]).sum())
     log(f"[mini draft rows] top1 differing {n_t}, conf differing {n_c} of {B * D}")
     assert n_t == 0 and n_c == 0
+
+
+def test_forward_end_to_end_mini(mini):
+    """All 20 blocks at full model size against the oracle's forward, the
+    residual stream carried from block to block with the combine's fused
+    next-block RMSNorm in between: batch 1, the first 32 prompt and 64 draft
+    tokens of the workload (its mask applied).  The GPU reports every block's
+    router logits and expert selection.  At every block: the selection is the
+    top-k of the GPU's own logits, and a token routed differently from the
+    oracle has an oracle k-th/(k+1)-th gap within twice that token's measured
+    router-logit error at that block (the same rule as the single-block tests;
+    over 20 blocks the error includes the bf16 drift the stream accumulates,
+    and flips of one token reach the others through attention).  Every token
+    routed alike at all 20 blocks matches the oracle's hidden state within
+    2e-2, its top-1 exactly outside the margin exemption, its max logit and
+    confidence within 2e-2."""
+    import torch
+    import oracle
+    w, R, W, toks = mini
+    s = w.model
+    P, D, d, E, k, L = 32, 64, s.d_model, s.n_experts, s.top_k, s.n_layers
+    t = np.concatenate([toks[:1, :P], toks[:1, w.prompt_len:w.prompt_len + D]], 1).astype(np.int32)
+    T = t.size
+    out = R.debug_forward(torch.tensor(t, device="cuda"), P, want_routes=True)
+    x_ref, infos, _ = oracle.forward(W, t, collect=True)
+    g_ids = _np(out["routes"]).reshape(L, T, k)
+    g_z = _np(out["router_logits"]).reshape(L, T, E).astype(np.float64)
+    o_z = np.stack([i["router_logits"].reshape(T, E) for i in infos])
+    o_ids = np.stack([i["route_ids"].reshape(T, k) for i in infos])
+    gaps = np.stack([i["route_gap"].reshape(T) for i in infos])                   # [L, T]
+    err = np.max(np.abs(g_z - o_z), -1)                                            # [L, T]
+    own = np.argsort(-g_z, axis=-1, kind="stable")[..., :k]
+    differs = np.any(np.sort(g_ids, -1) != np.sort(o_ids, -1), -1)                 # [L, T]
+    unexplained = differs & (gaps > 2 * err)
+    alike = ~np.any(differs, 0)
+    hid = _np(out["hidden"])
+    ref = x_ref.reshape(-1, d)
+    eh = max_abs_rel(hid[alike], ref[alike])
+    red = oracle.lm_head_reduce(W, x_ref[:, P:].reshape(-1, d))
+    keep_d = alike[P:] & (red["margin"] > MARGIN)
+    mism = int(np.sum((_np(out["top1"]) != red["top1"]) & keep_d))
+    em = max_abs_rel(_np(out["max_logit"])[keep_d], red["max_logit"][keep_d])
+    ec = float(np.max(np.abs(_np(out["conf"])[keep_d] - red["conf"][keep_d]))) if keep_d.any() else 0.0
+    log(f"[mini end to end] router-logit error per block (max over tokens): {np.round(err.max(1), 4).tolist()}; "
+        f"tokens routed differently per block: {differs.sum(1).tolist()}; {int(alike.sum())}/{T} routed alike "
+        f"at every block, hidden {eh:.2e} on them (all tokens {max_abs_rel(hid, ref):.2e}); top1 checked "
+        f"{int(keep_d.sum())} mismatches {mism}; max_logit {em:.2e}; conf {ec:.2e}")
+    assert np.array_equal(own, g_ids)
+    assert not unexplained.any(), np.argwhere(unexplained)[:8]
+    assert int(alike.sum()) >= T // 8
+    assert eh <= HIDDEN_TOL and em <= HIDDEN_TOL and ec <= HIDDEN_TOL
+    assert mism == 0
