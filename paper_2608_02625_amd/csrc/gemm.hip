@@ -20,6 +20,7 @@
 // workgroups round-robin) processes a contiguous range of tiles; within that
 // range dense GEMMs raster group_m row-tiles at a time to keep operands in L2.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "common.h"
@@ -28,6 +29,7 @@
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMaxDevices = 64;
 
 template <int BM, int BN, int BK, int SA, int SB, int NW>
 struct TileCfg {
@@ -950,15 +952,22 @@ hipError_t launch_t(const GemmArgs& a, int max_tiles, hipStream_t st) {
     } else {
     auto kernel = gemm_kernel<BM, BN, BK, SA, SB, NW, EPI, GROUPED, PP>;
     // Workgroups that fit on the device at once (a multiple of 8, one share
-    // per XCD); a persistent grid of at most that many walks all tiles.
-    static int resident = 0;
+    // per XCD), cached per device for this kernel; a persistent grid of at
+    // most that many walks all tiles.  Concurrent first calls compute the same
+    // value, so the relaxed atomic cache is race-free.
+    static std::atomic<int> resident_of[kMaxDevices];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int resident = resident_of[dev].load(std::memory_order_relaxed);
     if (resident == 0) {
-        int dev = 0, cus = 0, occ = 0;
-        hipError_t e = hipGetDevice(&dev);
-        if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        int cus = 0, occ = 0;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
         if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, NW * 64, 0);
         if (e != hipSuccess) return e;
         resident = std::max(8, cus * std::max(occ, 1) / 8 * 8);
+        resident_of[dev].store(resident, std::memory_order_relaxed);
     }
     const int tiles_n = (a.N + BN - 1) / BN;
     const int tiles_m = GROUPED ? max_tiles : (a.M + BM - 1) / BM;
