@@ -106,6 +106,68 @@ def kernel_flops(name, shape, B, P, D):
     raise KeyError(name)
 
 
+def library_reference(shape, B, P, D, launches, reps=20):
+    """The vendor libraries on the same shapes, for context: torch.matmul
+    (hipBLASLt; plain bf16 output, none of the fused epilogues) and torch's
+    scaled_dot_product_attention, each beside the per-launch time of the
+    library kernel doing that product in a refinement pass (`launches`: the
+    (kernel, ms) pairs of one profiled pass, in launch order).  The expert
+    GEMMs are set against one dense GEMM over all routed rows (no padding, no
+    gather), beside the mean launch of the blocks whose FFN runs on every row."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+
+    S, T, R = P + D, B * (P + D), B * D
+    d, hd, H, KV = shape.d_model, shape.head_dim, shape.n_heads, shape.n_kv_heads
+
+    def ours(name, first_n=None):
+        ms = [m for (n, m) in launches if n == name]
+        ms = ms[:first_n] if first_n else ms
+        return round(float(np.mean(ms)) * 1e3, 1) if ms else None
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    gemms = [("gemm_qkv", T, (H + 2 * KV) * hd, d), ("gemm_o", T, d, H * hd)]
+    if shape.n_experts:
+        kr = shape.top_k + shape.n_shared_experts
+        F_ = shape.expert_ffn_dim
+        gemms += [("gemm_expert_gate_up", T * kr, 2 * F_, d), ("gemm_expert_down", T * kr, d, F_)]
+    gemms.append(("gemm_lm_head", R, shape.vocab, d))
+    out = {}
+    for name, M, N, K in gemms:
+        a = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(N, K, device="cuda", dtype=torch.bfloat16)
+        us = timed(lambda: torch.matmul(a, b.t()))
+        del a, b
+        first = shape.n_layers - 1 if name.startswith("gemm_expert") and P > 0 else None
+        out[name] = {"library": "torch.matmul", "M": M, "N": N, "K": K, "library_us": round(us, 1),
+                     "library_tflops": round(2 * M * N * K / us / 1e6, 1), "ours_us": ours(name, first)}
+    q = torch.randn(B, H, S, hd, device="cuda", dtype=torch.bfloat16)
+    k = torch.randn(B, KV, S, hd, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn(B, KV, S, hd, device="cuda", dtype=torch.bfloat16)
+    try:
+        us = timed(lambda: F.scaled_dot_product_attention(q, k, v, enable_gqa=True))
+        out["attention"] = {"library": "scaled_dot_product_attention", "B": B, "H": H, "KV": KV, "S": S, "hd": hd,
+                            "library_us": round(us, 1), "library_tflops": round(4 * B * H * S * S * hd / us / 1e6, 1),
+                            "ours_us": ours("attention")}
+    except RuntimeError as e:                      # no fused attention kernel for this shape
+        out["attention"] = {"library": "scaled_dot_product_attention", "error": str(e)[:200],
+                            "ours_us": ours("attention")}
+    del q, k, v
+    return out
+
+
 def cpu_baseline(w, layers_sample=1):
     """Oracle time for one batch row: `layers_sample` layers + the LM-head
     reduction over that row's draft positions, extrapolated to all layers.
@@ -418,6 +480,8 @@ def main():
     ap.add_argument("--kernel", default="gemm_expert_gate_up", help="kernel reported in roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-table", action="store_true", help="also time every kernel (separate pass)")
+    ap.add_argument("--library-reference", action="store_true",
+                    help="also time torch.matmul / scaled_dot_product_attention on the pass's shapes")
     ap.add_argument("--local-span", type=int, default=0,
                     help="time local refinement instead: one pass over every draft chunk of this many tokens")
     ap.add_argument("--draft", action="store_true",
@@ -530,7 +594,7 @@ def main():
                      "traffic": recorded_traffic(args.kernel, w.name),
                      "launches": len(kt), "avg_ms": k_avg_ms, "flops_per_launch": k_flops},
     }
-    if args.kernel_table:
+    if args.kernel_table or args.library_reference:
         R.set_profiling("*")
         R.refine_step(tokens, P, w.threshold)
         rows = R.profile_read()
@@ -540,7 +604,11 @@ def main():
             a = agg.setdefault(n, [0, 0.0])
             a[0] += 1
             a[1] += ms
-        out["kernel_table_ms"] = {n: round(v[1], 4) for n, v in sorted(agg.items(), key=lambda kv: -kv[1][1])}
+        if args.kernel_table:
+            out["kernel_table_ms"] = {n: round(v[1], 4) for n, v in sorted(agg.items(), key=lambda kv: -kv[1][1])}
+        if args.library_reference:
+            print("[bench] timing the vendor libraries on the same shapes", file=sys.stderr, flush=True)
+            out["library_reference"] = library_reference(shape, B, P, D, rows)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)
