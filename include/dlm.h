@@ -39,7 +39,9 @@ typedef enum {
     DLM_ERR_INVALID_ARG = -1,   /* bad shape, null pointer, non-finite threshold ... */
     DLM_ERR_HIP = -3,           /* a HIP runtime call failed                          */
     DLM_ERR_UNSUPPORTED = -4,   /* a shape the kernels do not implement              */
-    DLM_ERR_WORKSPACE = -5      /* weights or workspace buffer too small             */
+    DLM_ERR_WORKSPACE = -5,     /* weights or workspace buffer too small             */
+    DLM_ERR_NO_MEMORY = -6,     /* a host memory allocation inside the library failed */
+    DLM_ERR_INTERNAL = -7       /* any other unexpected host-side failure            */
 } dlm_status;
 
 /*
@@ -408,6 +410,17 @@ dlm_status dlm_weight_info(dlm_model* m, int32_t layer_field, int32_t kind, int3
  */
 dlm_status dlm_set_profiling(dlm_model* m, const char* name_filter);
 int32_t dlm_profile_read(dlm_model* m, const char** names, float* ms, int32_t max_entries);
+
+/*
+ * Test hook for the library's own host allocations (plans, the model object,
+ * profiling records): the n-th allocation point passed from now fails as if
+ * the host were out of memory (n = 0: none).  The entry point that meets it
+ * returns DLM_ERR_NO_MEMORY with nothing half-built left behind (no model
+ * handle is returned; no kernel has been launched when a plan fails).  No
+ * C++ exception ever leaves an entry point.  n < 0 -> DLM_ERR_INVALID_ARG.
+ * Process-wide; for single-threaded tests.
+ */
+dlm_status dlm_debug_fail_host_alloc(int32_t n);
 
 void dlm_free(dlm_model* m);
 const char* dlm_last_error(void);

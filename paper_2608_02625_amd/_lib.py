@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "libdlm.so")
 DLM_OK = 0
 STATIC_SCRATCH_BYTES = 64 << 20      # DLM_STATIC_SCRATCH_BYTES of include/dlm.h
 STATUS_NAMES = {0: "DLM_OK", -1: "DLM_ERR_INVALID_ARG", -3: "DLM_ERR_HIP", -4: "DLM_ERR_UNSUPPORTED",
-                -5: "DLM_ERR_WORKSPACE"}
+                -5: "DLM_ERR_WORKSPACE", -6: "DLM_ERR_NO_MEMORY", -7: "DLM_ERR_INTERNAL"}
 
 
 class DlmConfig(ctypes.Structure):
@@ -90,6 +90,7 @@ SIGNATURES = [
     ("dlm_weight_info", _I, [_P, _I, _I, _I, ctypes.POINTER(_P), ctypes.POINTER(_I)]),
     ("dlm_set_profiling", _I, [_P, ctypes.c_char_p]),
     ("dlm_profile_read", _I, [_P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_F), _I]),
+    ("dlm_debug_fail_host_alloc", _I, [_I]),
     ("dlm_free", None, [_P]),
     ("dlm_last_error", ctypes.c_char_p, []),
 ]

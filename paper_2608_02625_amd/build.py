@@ -66,6 +66,62 @@ def build(jobs: int | None = None) -> str:
     return OUT
 
 
+# Host-code sanitizers: each flag goes to the host compilation only.
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def _clangxx() -> str:
+    for c in (os.path.join(os.path.dirname(os.path.realpath(_hipcc())), "..", "llvm", "bin", "clang++"),
+              "/opt/rocm/llvm/bin/clang++"):
+        if os.path.exists(c):
+            return os.path.realpath(c)
+    raise RuntimeError("clang++ of the ROCm toolchain not found")
+
+
+def build_host_sanitized() -> str:
+    """The library with the host code of its C ABI (engine.hip: argument
+    validation, planning, error paths) under AddressSanitizer and
+    UndefinedBehaviorSanitizer; the kernel sources' objects are those of
+    build(), and device code is never instrumented.  For CPU checks of the
+    host paths: load it in a process that preloads the ASan runtime
+    (asan_runtime())."""
+    out_dir = os.path.join(BUILD, "hostsan")
+    os.makedirs(out_dir, exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        if src != "engine.hip":
+            obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+            if not os.path.exists(obj):
+                _compile(src)
+            objs.append(obj)
+    obj = os.path.join(out_dir, "engine.o")
+    cmd = [_hipcc(), *CFLAGS, *SANITIZE, "-c", os.path.join(CSRC, "engine.hip"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized host build failed:\n{r.stderr}")
+    objs.append(obj)
+    out = os.path.join(out_dir, "libdlm_hostsan.so")
+    rocm = os.path.realpath(os.path.join(os.path.dirname(os.path.realpath(_hipcc())), ".."))
+    # The sanitizer runtime is not linked in: the loading process preloads it,
+    # and it resolves the objects' instrumentation calls.
+    cmd = [_clangxx(), "-shared", "-fPIC", *objs, "-L" + os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath," + os.path.join(rocm, "lib"), "-o", out]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized host link failed:\n{r.stderr}")
+    return out
+
+
+def asan_runtime() -> str:
+    """Path of the toolchain's shared ASan runtime (to preload)."""
+    r = subprocess.run([_clangxx(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    path = r.stdout.strip()
+    if r.returncode != 0 or not os.path.exists(path):
+        raise RuntimeError("ASan runtime not found")
+    return path
+
+
 if __name__ == "__main__":
     print(build())
     sys.exit(0)

@@ -17,6 +17,9 @@
 #include <algorithm>
 #include <chrono>
 #include <mutex>
+#include <atomic>
+#include <exception>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -30,6 +33,43 @@ thread_local std::string g_last_error;
 dlm_status fail(dlm_status s, const std::string& msg) {
     g_last_error = msg;
     return s;
+}
+
+// No C++ exception leaves an entry point: each catches what its body throws
+// (a failed host allocation in a plan's vectors, a message string or the
+// profiling records) and reports it as a status.  The message is set without
+// allocating when the string already holds enough capacity.
+void set_error_noexcept(const char* msg) noexcept {
+    try {
+        g_last_error.assign(msg);
+    } catch (...) {
+        g_last_error.clear();
+    }
+}
+
+dlm_status caught_exception() noexcept {
+    try {
+        throw;
+    } catch (const std::bad_alloc&) {
+        set_error_noexcept("a host memory allocation failed");
+        return DLM_ERR_NO_MEMORY;
+    } catch (const std::exception& e) {
+        set_error_noexcept(e.what());
+    } catch (...) {
+        set_error_noexcept("unexpected exception");
+    }
+    return DLM_ERR_INTERNAL;
+}
+
+// Test hook: the n-th pass through a host allocation point from now throws
+// std::bad_alloc (0: never).
+std::atomic<int> g_fail_alloc_in{0};
+
+void alloc_point() {
+    int v = g_fail_alloc_in.load(std::memory_order_relaxed);
+    while (v > 0 && !g_fail_alloc_in.compare_exchange_weak(v, v - 1, std::memory_order_relaxed)) {
+    }
+    if (v == 1) throw std::bad_alloc();
 }
 
 #define HIP_TRY(expr)                                                                         \
@@ -96,6 +136,7 @@ std::string validate(const dlm_config* c) {
 }
 
 WeightPlan plan_weights(const dlm_config& c) {
+    alloc_point();
     WeightPlan p;
     const int d = c.d_model, hd = c.head_dim, H = c.n_heads, KV = c.n_kv_heads;
     auto add = [&](uint64_t elems) {
@@ -295,8 +336,15 @@ void prof_begin(Ctx& x, const char* name) {
     if (!m->prof_on || x.no_events) return;
     if (!(m->prof_filter == "*" || m->prof_filter == name)) return;
     if (m->prof_used == m->prof.size()) {
+        alloc_point();
+        if (m->prof.size() == m->prof.capacity())   // may throw: before the events exist
+            m->prof.reserve(2 * m->prof.size() + 64);
         ProfRec r{name, nullptr, nullptr};
-        if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return;
+        if (hipEventCreate(&r.a) != hipSuccess) return;
+        if (hipEventCreate(&r.b) != hipSuccess) {
+            (void)hipEventDestroy(r.a);
+            return;
+        }
         m->prof.push_back(r);
     }
     ProfRec& r = m->prof[m->prof_used];
@@ -740,160 +788,195 @@ extern "C" {
 const char* dlm_last_error(void) { return g_last_error.c_str(); }
 
 size_t dlm_weights_bytes(const dlm_config* cfg) {
-    if (!validate(cfg).empty()) return 0;
-    return plan_weights(*cfg).total;
+    try {
+        if (!validate(cfg).empty()) return 0;
+        return plan_weights(*cfg).total;
+    } catch (...) {
+        caught_exception();
+        return 0;
+    }
 }
 
 size_t dlm_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len) {
-    if (!validate(cfg).empty() || !check_shape(batch, prompt_len, draft_len).empty()) return 0;
-    if (!check_offsets(*cfg, (int64_t)batch * (prompt_len + draft_len)).empty()) return 0;
-    return plan_workspace(*cfg, batch, prompt_len, draft_len).total;
+    try {
+        if (!validate(cfg).empty() || !check_shape(batch, prompt_len, draft_len).empty()) return 0;
+        if (!check_offsets(*cfg, (int64_t)batch * (prompt_len + draft_len)).empty()) return 0;
+        return plan_workspace(*cfg, batch, prompt_len, draft_len).total;
+    } catch (...) {
+        caught_exception();
+        return 0;
+    }
 }
 
 dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void* d_weights,
                                       size_t weights_bytes, void* hip_stream, dlm_model** out) {
-    const std::string e = validate(cfg);
-    if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
-    if (!out) return fail(DLM_ERR_INVALID_ARG, "out is NULL");
-    *out = nullptr;
-    if (!d_weights) return fail(DLM_ERR_INVALID_ARG, "weights buffer is NULL");
-    if (((uintptr_t)d_weights) % kAlign) return fail(DLM_ERR_INVALID_ARG, "weights buffer must be 256-byte aligned");
-    WeightPlan plan = plan_weights(*cfg);
-    if (weights_bytes < plan.total)
-        return fail(DLM_ERR_WORKSPACE, "weights buffer too small: need " + std::to_string(plan.total) + " bytes");
-    char* scratch_ptr = nullptr;
-    int dev = 0;
-    TRY(scratch_on_current_device(&scratch_ptr, &dev));     // set-up: once per device
-    hipStream_t st = (hipStream_t)hip_stream;
-    char* base = (char*)d_weights;
-    for (const TensorInit& t : plan.inits) {
-        bf16_t* dst = reinterpret_cast<bf16_t*>(base + t.off);
-        if (t.kind_fill) {
-            launch_fill_bf16(dst, t.n_phys, (bf16_t)0x3f80, st);
-        } else {
-            const float c = (float)((double)cfg->init_std * (double)t.scale * sqrt(3.0) / 65536.0);
-            launch_init_weights(dst, t.n_phys, t.cols, t.tid_a, t.tid_b, t.layout, seed, c, st);
+    try {
+        const std::string e = validate(cfg);
+        if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
+        if (!out) return fail(DLM_ERR_INVALID_ARG, "out is NULL");
+        *out = nullptr;
+        if (!d_weights) return fail(DLM_ERR_INVALID_ARG, "weights buffer is NULL");
+        if (((uintptr_t)d_weights) % kAlign) return fail(DLM_ERR_INVALID_ARG, "weights buffer must be 256-byte aligned");
+        WeightPlan plan = plan_weights(*cfg);
+        if (weights_bytes < plan.total)
+            return fail(DLM_ERR_WORKSPACE, "weights buffer too small: need " + std::to_string(plan.total) + " bytes");
+        char* scratch_ptr = nullptr;
+        int dev = 0;
+        TRY(scratch_on_current_device(&scratch_ptr, &dev));     // set-up: once per device
+        hipStream_t st = (hipStream_t)hip_stream;
+        char* base = (char*)d_weights;
+        for (const TensorInit& t : plan.inits) {
+            bf16_t* dst = reinterpret_cast<bf16_t*>(base + t.off);
+            if (t.kind_fill) {
+                launch_fill_bf16(dst, t.n_phys, (bf16_t)0x3f80, st);
+            } else {
+                const float c = (float)((double)cfg->init_std * (double)t.scale * sqrt(3.0) / 65536.0);
+                launch_init_weights(dst, t.n_phys, t.cols, t.tid_a, t.tid_b, t.layout, seed, c, st);
+            }
+            HIP_TRY(hipGetLastError());
         }
-        HIP_TRY(hipGetLastError());
+        alloc_point();
+        dlm_model* m = new dlm_model();
+        m->cfg = *cfg;
+        m->seed = seed;
+        m->device = dev;
+        m->scratch = scratch_ptr;
+        m->base = base;
+        m->bytes = weights_bytes;
+        m->plan = std::move(plan);
+        *out = m;
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
     }
-    dlm_model* m = new dlm_model();
-    m->cfg = *cfg;
-    m->seed = seed;
-    m->device = dev;
-    m->scratch = scratch_ptr;
-    m->base = base;
-    m->bytes = weights_bytes;
-    m->plan = std::move(plan);
-    *out = m;
-    return DLM_OK;
 }
 
 dlm_status dlm_refine_step_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                               int32_t* d_tokens, const dlm_edit_rule* rule, void* d_workspace,
                               size_t workspace_bytes, void* hip_stream, int32_t* d_top1, float* d_conf,
                               dlm_stats* d_stats, int32_t* d_eos_written) {
-    Workspace w;
-    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
-    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
-    TRY(check_rule(m->cfg, rule));
-    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
-    return step_impl(x, d_tokens, *rule, d_top1, d_conf, d_stats, d_eos_written);
+    try {
+        Workspace w;
+        TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+        if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+        TRY(check_rule(m->cfg, rule));
+        Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+        return step_impl(x, d_tokens, *rule, d_top1, d_conf, d_stats, d_eos_written);
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                            int32_t* d_tokens, float threshold, void* d_workspace, size_t workspace_bytes,
                            void* hip_stream, int32_t* d_top1, float* d_conf, dlm_stats* d_stats) {
-    const dlm_edit_rule rule{threshold, threshold, -1};
-    return dlm_refine_step_ex(m, batch, prompt_len, draft_len, d_tokens, &rule, d_workspace, workspace_bytes,
-                              hip_stream, d_top1, d_conf, d_stats, nullptr);
+    try {
+        const dlm_edit_rule rule{threshold, threshold, -1};
+        return dlm_refine_step_ex(m, batch, prompt_len, draft_len, d_tokens, &rule, d_workspace, workspace_bytes,
+                                  hip_stream, d_top1, d_conf, d_stats, nullptr);
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_refine_step_static(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                                   int32_t* d_tokens, float threshold, void* hip_stream, int32_t* d_top1,
                                   float* d_conf, dlm_stats* d_stats) {
-    if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
-    std::string e = check_shape(batch, prompt_len, draft_len);
-    if (e.empty()) e = check_offsets(m->cfg, (int64_t)batch * (prompt_len + draft_len));
-    if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
-    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
-    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
-    int dev = -1;
-    HIP_TRY(hipGetDevice(&dev));
-    if (dev != m->device || !m->scratch)
-        return fail(DLM_ERR_INVALID_ARG, "the model's device (current when its weights were loaded) must be current");
-    const Workspace w = plan_workspace(m->cfg, batch, prompt_len, draft_len);
-    if (w.total > (size_t)DLM_STATIC_SCRATCH_BYTES)
-        return fail(DLM_ERR_WORKSPACE, "this shape needs " + std::to_string(w.total) +
-                                           " bytes of workspace; the static scratch holds " +
-                                           std::to_string((size_t)DLM_STATIC_SCRATCH_BYTES));
-    // Every buffer the pass reads before writing it in the same pass (the
-    // counters, the V^T padding) is cleared by a kernel of the pass itself,
-    // so whatever an earlier call left in the scratch does not matter.
-    const dlm_edit_rule rule{threshold, threshold, -1};
-    Ctx x = ctx_for(m, batch, prompt_len, draft_len, m->scratch, w, hip_stream);
-    x.no_events = true;
-    return step_impl(x, d_tokens, rule, d_top1, d_conf, d_stats, nullptr);
+    try {
+        if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+        std::string e = check_shape(batch, prompt_len, draft_len);
+        if (e.empty()) e = check_offsets(m->cfg, (int64_t)batch * (prompt_len + draft_len));
+        if (!e.empty()) return fail(DLM_ERR_INVALID_ARG, e);
+        if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+        if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+        int dev = -1;
+        HIP_TRY(hipGetDevice(&dev));
+        if (dev != m->device || !m->scratch)
+            return fail(DLM_ERR_INVALID_ARG, "the model's device (current when its weights were loaded) must be current");
+        const Workspace w = plan_workspace(m->cfg, batch, prompt_len, draft_len);
+        if (w.total > (size_t)DLM_STATIC_SCRATCH_BYTES)
+            return fail(DLM_ERR_WORKSPACE, "this shape needs " + std::to_string(w.total) +
+                                               " bytes of workspace; the static scratch holds " +
+                                               std::to_string((size_t)DLM_STATIC_SCRATCH_BYTES));
+        // Every buffer the pass reads before writing it in the same pass (the
+        // counters, the V^T padding) is cleared by a kernel of the pass itself,
+        // so whatever an earlier call left in the scratch does not matter.
+        const dlm_edit_rule rule{threshold, threshold, -1};
+        Ctx x = ctx_for(m, batch, prompt_len, draft_len, m->scratch, w, hip_stream);
+        x.no_events = true;
+        return step_impl(x, d_tokens, rule, d_top1, d_conf, d_stats, nullptr);
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_refine_ex(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                          const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
                          const dlm_edit_rule* rule, void* d_workspace, size_t workspace_bytes,
                          void* hip_stream, dlm_stats* h_stats, int32_t* h_stop_reason) {
-    Workspace w;
-    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
-    if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
-    if (n_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_steps < 0");
-    TRY(check_rule(m->cfg, rule));
-    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
-    int32_t* tokens = x.at<int32_t>(w.tokens);
-    int32_t* counters = x.at<int32_t>(w.counters);
-    launch_apply_mask(d_prompt, d_draft, d_mask, tokens, batch, prompt_len, draft_len, m->cfg.mask_id, x.st);
-    HIP_TRY(hipGetLastError());
-    dlm_stats tot{0, 0, 0, 0, 0};
-    int32_t reason = 0;
-    for (int s = 0; s < n_steps; ++s) {
-        TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
-        int32_t st[CNT_WORDS] = {};                   // the pass counters
-        HIP_TRY(hipMemcpyAsync(st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
+    try {
+        Workspace w;
+        TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+        if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
+        if (n_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_steps < 0");
+        TRY(check_rule(m->cfg, rule));
+        Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+        int32_t* tokens = x.at<int32_t>(w.tokens);
+        int32_t* counters = x.at<int32_t>(w.counters);
+        launch_apply_mask(d_prompt, d_draft, d_mask, tokens, batch, prompt_len, draft_len, m->cfg.mask_id, x.st);
+        HIP_TRY(hipGetLastError());
+        dlm_stats tot{0, 0, 0, 0, 0};
+        int32_t reason = 0;
+        for (int s = 0; s < n_steps; ++s) {
+            TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
+            int32_t st[CNT_WORDS] = {};                   // the pass counters
+            HIP_TRY(hipMemcpyAsync(st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
+            HIP_TRY(hipStreamSynchronize(x.st));
+            if (st[CNT_INVALID]) return fail_invalid_tokens(st[CNT_INVALID]);
+            tot.n_unmasked += st[CNT_UNMASKED];
+            tot.n_edited += st[CNT_EDITED];
+            tot.steps_run += 1;
+            if (st[CNT_UNMASKED] + st[CNT_EDITED] == 0) {
+                reason = 1;
+                break;
+            }
+            if (rule->eos_id >= 0 && st[CNT_EOS] > 0) {
+                reason = 2;
+                break;
+            }
+        }
+        launch_copy_draft_out(tokens, d_draft, batch, x.S, prompt_len, draft_len, x.st);
+        launch_zero_i32(counters, 4, x.st);
+        launch_count_masks(tokens, batch, x.S, prompt_len, draft_len, m->cfg.mask_id, counters + 2, x.st);
+        HIP_TRY(hipGetLastError());
+        dlm_stats st{};
+        HIP_TRY(hipMemcpyAsync(&st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
         HIP_TRY(hipStreamSynchronize(x.st));
-        if (st[CNT_INVALID]) return fail_invalid_tokens(st[CNT_INVALID]);
-        tot.n_unmasked += st[CNT_UNMASKED];
-        tot.n_edited += st[CNT_EDITED];
-        tot.steps_run += 1;
-        if (st[CNT_UNMASKED] + st[CNT_EDITED] == 0) {
-            reason = 1;
-            break;
-        }
-        if (rule->eos_id >= 0 && st[CNT_EOS] > 0) {
-            reason = 2;
-            break;
-        }
+        tot.n_masked_left = st.n_masked_left;
+        if (h_stats) *h_stats = tot;
+        if (h_stop_reason) *h_stop_reason = reason;
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
     }
-    launch_copy_draft_out(tokens, d_draft, batch, x.S, prompt_len, draft_len, x.st);
-    launch_zero_i32(counters, 4, x.st);
-    launch_count_masks(tokens, batch, x.S, prompt_len, draft_len, m->cfg.mask_id, counters + 2, x.st);
-    HIP_TRY(hipGetLastError());
-    dlm_stats st{};
-    HIP_TRY(hipMemcpyAsync(&st, counters, sizeof(st), hipMemcpyDeviceToHost, x.st));
-    HIP_TRY(hipStreamSynchronize(x.st));
-    tot.n_masked_left = st.n_masked_left;
-    if (h_stats) *h_stats = tot;
-    if (h_stop_reason) *h_stop_reason = reason;
-    return DLM_OK;
 }
 
 dlm_status dlm_refine_step_span(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t span_len,
                                 int32_t span_start, int32_t* d_tokens, const dlm_edit_rule* rule, void* d_workspace,
                                 size_t workspace_bytes, void* hip_stream, int32_t* d_top1, float* d_conf,
                                 dlm_stats* d_stats, int32_t* d_eos_written) {
-    Workspace w;
-    TRY(check_common(m, batch, prompt_len, span_len, d_workspace, workspace_bytes, &w));
-    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
-    if (span_start < 0) return fail(DLM_ERR_INVALID_ARG, "span_start < 0");
-    TRY(check_rule(m->cfg, rule));
-    Ctx x = ctx_for(m, batch, prompt_len, span_len, d_workspace, w, hip_stream);
-    x.pos_shift = span_start;
-    return step_impl(x, d_tokens, *rule, d_top1, d_conf, d_stats, d_eos_written);
+    try {
+        Workspace w;
+        TRY(check_common(m, batch, prompt_len, span_len, d_workspace, workspace_bytes, &w));
+        if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+        if (span_start < 0) return fail(DLM_ERR_INVALID_ARG, "span_start < 0");
+        TRY(check_rule(m->cfg, rule));
+        Ctx x = ctx_for(m, batch, prompt_len, span_len, d_workspace, w, hip_stream);
+        x.pos_shift = span_start;
+        return step_impl(x, d_tokens, *rule, d_top1, d_conf, d_stats, d_eos_written);
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
@@ -901,335 +984,400 @@ dlm_status dlm_refine_local(dlm_model* m, int32_t batch, int32_t prompt_len, int
                             const int32_t* h_span, const int32_t* h_passes, const dlm_edit_rule* rule,
                             void* d_workspace, size_t workspace_bytes, void* hip_stream, dlm_stats* h_stats,
                             int32_t* h_stop_reason) {
-    Workspace wfull;
-    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &wfull));
-    if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
-    if (n_stages < 0 || (n_stages > 0 && (!h_span || !h_passes))) return fail(DLM_ERR_INVALID_ARG, "bad schedule");
-    for (int i = 0; i < n_stages; ++i)
-        if (h_span[i] < 1 || h_passes[i] < 0) return fail(DLM_ERR_INVALID_ARG, "span < 1 or passes < 0");
-    TRY(check_rule(m->cfg, rule));
-    hipStream_t st = (hipStream_t)hip_stream;
-    const int n = batch * draft_len;
-    if (d_mask) launch_mask_draft(d_draft, d_mask, n, m->cfg.mask_id, st);
-    HIP_TRY(hipGetLastError());
-    dlm_stats tot{0, 0, 0, 0, 0};
-    int32_t reason = 1;                                // every chunk stopped on its own (or nothing ran)
-    bool eos_stop = false;
-    for (int g = 0; g < n_stages && !eos_stop; ++g) {
-        const int L = std::min<int>(h_span[g], draft_len);
-        for (int c0 = 0; c0 < draft_len && !eos_stop; c0 += L) {
-            const int len = std::min(L, draft_len - c0);
-            Workspace w;
-            TRY(check_common(m, batch, prompt_len, len, d_workspace, workspace_bytes, &w));
-            Ctx x = ctx_for(m, batch, prompt_len, len, d_workspace, w, hip_stream);
-            x.pos_shift = c0;
-            int32_t* tokens = x.at<int32_t>(w.tokens);
-            int32_t* counters = x.at<int32_t>(w.counters);
-            launch_span_gather(d_prompt, d_draft, tokens, batch, prompt_len, draft_len, c0, len, st);
-            HIP_TRY(hipGetLastError());
-            bool still = false;
-            for (int p = 0; p < h_passes[g]; ++p) {
-                TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
-                int32_t c[CNT_WORDS] = {};
-                HIP_TRY(hipMemcpyAsync(c, counters, sizeof(c), hipMemcpyDeviceToHost, st));
-                HIP_TRY(hipStreamSynchronize(st));
-                if (c[CNT_INVALID]) return fail_invalid_tokens(c[CNT_INVALID]);
-                tot.n_unmasked += c[CNT_UNMASKED];
-                tot.n_edited += c[CNT_EDITED];
-                tot.steps_run += 1;
-                if (c[CNT_UNMASKED] + c[CNT_EDITED] == 0) {
-                    still = true;
-                    break;
+    try {
+        Workspace wfull;
+        TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &wfull));
+        if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
+        if (n_stages < 0 || (n_stages > 0 && (!h_span || !h_passes))) return fail(DLM_ERR_INVALID_ARG, "bad schedule");
+        for (int i = 0; i < n_stages; ++i)
+            if (h_span[i] < 1 || h_passes[i] < 0) return fail(DLM_ERR_INVALID_ARG, "span < 1 or passes < 0");
+        TRY(check_rule(m->cfg, rule));
+        hipStream_t st = (hipStream_t)hip_stream;
+        const int n = batch * draft_len;
+        if (d_mask) launch_mask_draft(d_draft, d_mask, n, m->cfg.mask_id, st);
+        HIP_TRY(hipGetLastError());
+        dlm_stats tot{0, 0, 0, 0, 0};
+        int32_t reason = 1;                                // every chunk stopped on its own (or nothing ran)
+        bool eos_stop = false;
+        for (int g = 0; g < n_stages && !eos_stop; ++g) {
+            const int L = std::min<int>(h_span[g], draft_len);
+            for (int c0 = 0; c0 < draft_len && !eos_stop; c0 += L) {
+                const int len = std::min(L, draft_len - c0);
+                Workspace w;
+                TRY(check_common(m, batch, prompt_len, len, d_workspace, workspace_bytes, &w));
+                Ctx x = ctx_for(m, batch, prompt_len, len, d_workspace, w, hip_stream);
+                x.pos_shift = c0;
+                int32_t* tokens = x.at<int32_t>(w.tokens);
+                int32_t* counters = x.at<int32_t>(w.counters);
+                launch_span_gather(d_prompt, d_draft, tokens, batch, prompt_len, draft_len, c0, len, st);
+                HIP_TRY(hipGetLastError());
+                bool still = false;
+                for (int p = 0; p < h_passes[g]; ++p) {
+                    TRY(step_impl(x, tokens, *rule, nullptr, nullptr, nullptr));
+                    int32_t c[CNT_WORDS] = {};
+                    HIP_TRY(hipMemcpyAsync(c, counters, sizeof(c), hipMemcpyDeviceToHost, st));
+                    HIP_TRY(hipStreamSynchronize(st));
+                    if (c[CNT_INVALID]) return fail_invalid_tokens(c[CNT_INVALID]);
+                    tot.n_unmasked += c[CNT_UNMASKED];
+                    tot.n_edited += c[CNT_EDITED];
+                    tot.steps_run += 1;
+                    if (c[CNT_UNMASKED] + c[CNT_EDITED] == 0) {
+                        still = true;
+                        break;
+                    }
+                    if (rule->eos_id >= 0 && c[CNT_EOS] > 0) {
+                        eos_stop = true;
+                        break;
+                    }
                 }
-                if (rule->eos_id >= 0 && c[CNT_EOS] > 0) {
-                    eos_stop = true;
-                    break;
-                }
+                if (!still && h_passes[g] > 0) reason = reason == 2 ? 2 : 0;
+                launch_span_scatter(tokens, d_draft, batch, prompt_len, draft_len, c0, len, st);
+                HIP_TRY(hipGetLastError());
             }
-            if (!still && h_passes[g] > 0) reason = reason == 2 ? 2 : 0;
-            launch_span_scatter(tokens, d_draft, batch, prompt_len, draft_len, c0, len, st);
-            HIP_TRY(hipGetLastError());
         }
+        if (eos_stop) reason = 2;
+        int32_t* counters = reinterpret_cast<int32_t*>((char*)d_workspace + wfull.counters);
+        launch_zero_i32(counters, 4, st);
+        launch_count_masks(d_draft, batch, draft_len, 0, draft_len, m->cfg.mask_id, counters + 2, st);
+        HIP_TRY(hipGetLastError());
+        dlm_stats fin{};
+        HIP_TRY(hipMemcpyAsync(&fin, counters, sizeof(fin), hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipStreamSynchronize(st));
+        tot.n_masked_left = fin.n_masked_left;
+        if (h_stats) *h_stats = tot;
+        if (h_stop_reason) *h_stop_reason = reason;
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
     }
-    if (eos_stop) reason = 2;
-    int32_t* counters = reinterpret_cast<int32_t*>((char*)d_workspace + wfull.counters);
-    launch_zero_i32(counters, 4, st);
-    launch_count_masks(d_draft, batch, draft_len, 0, draft_len, m->cfg.mask_id, counters + 2, st);
-    HIP_TRY(hipGetLastError());
-    dlm_stats fin{};
-    HIP_TRY(hipMemcpyAsync(&fin, counters, sizeof(fin), hipMemcpyDeviceToHost, st));
-    HIP_TRY(hipStreamSynchronize(st));
-    tot.n_masked_left = fin.n_masked_left;
-    if (h_stats) *h_stats = tot;
-    if (h_stop_reason) *h_stop_reason = reason;
-    return DLM_OK;
 }
 
 dlm_status dlm_refine(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                       const int32_t* d_prompt, int32_t* d_draft, const uint8_t* d_mask, int32_t n_steps,
                       float threshold, void* d_workspace, size_t workspace_bytes, void* hip_stream,
                       dlm_stats* h_stats) {
-    const dlm_edit_rule rule{threshold, threshold, -1};
-    return dlm_refine_ex(m, batch, prompt_len, draft_len, d_prompt, d_draft, d_mask, n_steps, &rule, d_workspace,
-                         workspace_bytes, hip_stream, h_stats, nullptr);
+    try {
+        const dlm_edit_rule rule{threshold, threshold, -1};
+        return dlm_refine_ex(m, batch, prompt_len, draft_len, d_prompt, d_draft, d_mask, n_steps, &rule, d_workspace,
+                             workspace_bytes, hip_stream, h_stats, nullptr);
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 size_t dlm_draft_workspace_bytes(const dlm_config* cfg, int32_t batch, int32_t prompt_len, int32_t draft_len,
                                  int32_t block_len) {
-    if (!validate(cfg).empty() || !check_draft_shape(batch, prompt_len, draft_len, block_len).empty()) return 0;
-    if (!check_offsets(*cfg, (int64_t)batch * (prompt_len + draft_len)).empty()) return 0;
-    return plan_draft(*cfg, batch, prompt_len, draft_len, block_len).total;
+    try {
+        if (!validate(cfg).empty() || !check_draft_shape(batch, prompt_len, draft_len, block_len).empty()) return 0;
+        if (!check_offsets(*cfg, (int64_t)batch * (prompt_len + draft_len)).empty()) return 0;
+        return plan_draft(*cfg, batch, prompt_len, draft_len, block_len).total;
+    } catch (...) {
+        caught_exception();
+        return 0;
+    }
 }
 
 dlm_status dlm_draft_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, int32_t block_len,
                           int32_t block_index, int32_t steps_left, float threshold, int32_t* d_tokens,
                           void* d_workspace, size_t workspace_bytes, void* hip_stream, int32_t* d_top1,
                           float* d_conf, float* d_max_logit, dlm_stats* d_stats) {
-    DraftPlan p;
-    TRY(check_draft(m, batch, prompt_len, draft_len, block_len, d_workspace, workspace_bytes, &p));
-    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
-    const int n_blocks = (draft_len + block_len - 1) / block_len;
-    if (block_index < 0 || block_index >= n_blocks) return fail(DLM_ERR_INVALID_ARG, "block_index out of range");
-    if (steps_left < 1) return fail(DLM_ERR_INVALID_ARG, "steps_left < 1");
-    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
-    const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len,
-                     prompt_len + draft_len, block_len};
-    launch_zero_i32(dr.counters(), CNT_WORDS, dr.st);
-    TRY(dr.begin(d_tokens));
-    for (int j = 0; j < block_index; ++j) TRY(dr.run(d_tokens, dr.block_start(j), block_len, false));
-    TRY(dr.step(d_tokens, block_index, threshold, steps_left, d_top1, d_conf));
-    if (d_stats) HIP_TRY(hipMemcpyAsync(d_stats, dr.counters(), sizeof(dlm_stats), hipMemcpyDeviceToDevice, dr.st));
-    if (d_max_logit)
-        HIP_TRY(hipMemcpyAsync(d_max_logit, dr.ws + p.w.maxlogit, (size_t)batch * dr.block_rows(block_index) * 4,
-                               hipMemcpyDeviceToDevice, dr.st));
-    return DLM_OK;
+    try {
+        DraftPlan p;
+        TRY(check_draft(m, batch, prompt_len, draft_len, block_len, d_workspace, workspace_bytes, &p));
+        if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+        const int n_blocks = (draft_len + block_len - 1) / block_len;
+        if (block_index < 0 || block_index >= n_blocks) return fail(DLM_ERR_INVALID_ARG, "block_index out of range");
+        if (steps_left < 1) return fail(DLM_ERR_INVALID_ARG, "steps_left < 1");
+        if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+        const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len,
+                         prompt_len + draft_len, block_len};
+        launch_zero_i32(dr.counters(), CNT_WORDS, dr.st);
+        TRY(dr.begin(d_tokens));
+        for (int j = 0; j < block_index; ++j) TRY(dr.run(d_tokens, dr.block_start(j), block_len, false));
+        TRY(dr.step(d_tokens, block_index, threshold, steps_left, d_top1, d_conf));
+        if (d_stats) HIP_TRY(hipMemcpyAsync(d_stats, dr.counters(), sizeof(dlm_stats), hipMemcpyDeviceToDevice, dr.st));
+        if (d_max_logit)
+            HIP_TRY(hipMemcpyAsync(d_max_logit, dr.ws + p.w.maxlogit, (size_t)batch * dr.block_rows(block_index) * 4,
+                                   hipMemcpyDeviceToDevice, dr.st));
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_draft(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, const int32_t* d_prompt,
                      int32_t* d_draft, int32_t block_len, int32_t steps_per_block, float threshold,
                      void* d_workspace, size_t workspace_bytes, void* hip_stream, dlm_stats* h_stats,
                      int32_t* h_block_steps) {
-    DraftPlan p;
-    TRY(check_draft(m, batch, prompt_len, draft_len, block_len, d_workspace, workspace_bytes, &p));
-    if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
-    if (steps_per_block < 1) return fail(DLM_ERR_INVALID_ARG, "steps_per_block < 1");
-    if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
-    const int S = prompt_len + draft_len;
-    const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len, S, block_len};
-    int32_t* tokens = reinterpret_cast<int32_t*>((char*)d_workspace + p.tokens);
-    launch_zero_i32(dr.counters(), CNT_WORDS, dr.st);
-    launch_draft_init(d_prompt, tokens, batch, prompt_len, S, m->cfg.vocab, m->cfg.mask_id, dr.counters(), dr.st);
-    HIP_TRY(hipGetLastError());
-    TRY(dr.begin(tokens));
-    const int n_blocks = (draft_len + block_len - 1) / block_len;
-    dlm_stats tot{0, 0, 0, 0, 0};
-    for (int k = 0; k < n_blocks; ++k) {
-        int used = 0;
-        for (int t = 0; t < steps_per_block; ++t) {
-            // the first step of a block also commits the previous block's K/V
-            TRY(dr.step(tokens, k, threshold, steps_per_block - t, nullptr, nullptr, t == 0 && k > 0));
-            int32_t c[CNT_WORDS] = {};
-            HIP_TRY(hipMemcpyAsync(c, dr.counters(), sizeof(c), hipMemcpyDeviceToHost, dr.st));
-            HIP_TRY(hipStreamSynchronize(dr.st));
-            if (c[CNT_INVALID]) return fail_invalid_tokens(c[CNT_INVALID]);
-            ++used;
-            tot.n_unmasked += c[0];
-            if (c[2] == 0) break;                     // no [MASK] left in the block
+    try {
+        DraftPlan p;
+        TRY(check_draft(m, batch, prompt_len, draft_len, block_len, d_workspace, workspace_bytes, &p));
+        if (!d_draft || (prompt_len > 0 && !d_prompt)) return fail(DLM_ERR_INVALID_ARG, "prompt/draft is NULL");
+        if (steps_per_block < 1) return fail(DLM_ERR_INVALID_ARG, "steps_per_block < 1");
+        if (isnan(threshold)) return fail(DLM_ERR_INVALID_ARG, "threshold is NaN");
+        const int S = prompt_len + draft_len;
+        const Drafter dr{m, (char*)d_workspace, p, (hipStream_t)hip_stream, batch, prompt_len, draft_len, S, block_len};
+        int32_t* tokens = reinterpret_cast<int32_t*>((char*)d_workspace + p.tokens);
+        launch_zero_i32(dr.counters(), CNT_WORDS, dr.st);
+        launch_draft_init(d_prompt, tokens, batch, prompt_len, S, m->cfg.vocab, m->cfg.mask_id, dr.counters(), dr.st);
+        HIP_TRY(hipGetLastError());
+        TRY(dr.begin(tokens));
+        const int n_blocks = (draft_len + block_len - 1) / block_len;
+        dlm_stats tot{0, 0, 0, 0, 0};
+        for (int k = 0; k < n_blocks; ++k) {
+            int used = 0;
+            for (int t = 0; t < steps_per_block; ++t) {
+                // the first step of a block also commits the previous block's K/V
+                TRY(dr.step(tokens, k, threshold, steps_per_block - t, nullptr, nullptr, t == 0 && k > 0));
+                int32_t c[CNT_WORDS] = {};
+                HIP_TRY(hipMemcpyAsync(c, dr.counters(), sizeof(c), hipMemcpyDeviceToHost, dr.st));
+                HIP_TRY(hipStreamSynchronize(dr.st));
+                if (c[CNT_INVALID]) return fail_invalid_tokens(c[CNT_INVALID]);
+                ++used;
+                tot.n_unmasked += c[0];
+                if (c[2] == 0) break;                     // no [MASK] left in the block
+            }
+            tot.steps_run += used;
+            if (h_block_steps) h_block_steps[k] = used;
         }
-        tot.steps_run += used;
-        if (h_block_steps) h_block_steps[k] = used;
+        launch_copy_draft_out(tokens, d_draft, batch, S, prompt_len, draft_len, dr.st);
+        launch_zero_i32(dr.counters(), 4, dr.st);
+        launch_count_masks(tokens, batch, S, prompt_len, draft_len, m->cfg.mask_id, dr.counters() + 2, dr.st);
+        HIP_TRY(hipGetLastError());
+        dlm_stats fin{};
+        HIP_TRY(hipMemcpyAsync(&fin, dr.counters(), sizeof(fin), hipMemcpyDeviceToHost, dr.st));
+        HIP_TRY(hipStreamSynchronize(dr.st));
+        tot.n_masked_left = fin.n_masked_left;
+        if (h_stats) *h_stats = tot;
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
     }
-    launch_copy_draft_out(tokens, d_draft, batch, S, prompt_len, draft_len, dr.st);
-    launch_zero_i32(dr.counters(), 4, dr.st);
-    launch_count_masks(tokens, batch, S, prompt_len, draft_len, m->cfg.mask_id, dr.counters() + 2, dr.st);
-    HIP_TRY(hipGetLastError());
-    dlm_stats fin{};
-    HIP_TRY(hipMemcpyAsync(&fin, dr.counters(), sizeof(fin), hipMemcpyDeviceToHost, dr.st));
-    HIP_TRY(hipStreamSynchronize(dr.st));
-    tot.n_masked_left = fin.n_masked_left;
-    if (h_stats) *h_stats = tot;
-    return DLM_OK;
 }
 
 size_t dlm_cascade_workspace_bytes(const dlm_config* drafter_cfg, const dlm_config* refiner_cfg, int32_t batch,
                                    int32_t prompt_len, int32_t draft_len, int32_t block_len) {
-    const size_t a = dlm_draft_workspace_bytes(drafter_cfg, batch, prompt_len, draft_len, block_len);
-    const size_t b = dlm_workspace_bytes(refiner_cfg, batch, prompt_len, draft_len);
-    return a && b ? std::max(a, b) : 0;
+    try {
+        const size_t a = dlm_draft_workspace_bytes(drafter_cfg, batch, prompt_len, draft_len, block_len);
+        const size_t b = dlm_workspace_bytes(refiner_cfg, batch, prompt_len, draft_len);
+        return a && b ? std::max(a, b) : 0;
+    } catch (...) {
+        caught_exception();
+        return 0;
+    }
 }
 
 dlm_status dlm_cascade(dlm_model* drafter, dlm_model* refiner, int32_t batch, int32_t prompt_len, int32_t draft_len,
                        const int32_t* d_prompt, int32_t* d_draft, int32_t block_len, int32_t steps_per_block,
                        float draft_threshold, int32_t n_refine_steps, const dlm_edit_rule* rule, void* d_workspace,
                        size_t workspace_bytes, void* hip_stream, dlm_cascade_stats* h_stats) {
-    if (!drafter || !refiner) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
-    if (drafter->cfg.vocab != refiner->cfg.vocab || drafter->cfg.mask_id != refiner->cfg.mask_id)
-        return fail(DLM_ERR_INVALID_ARG, "drafter and refiner must share the vocabulary and the mask id");
-    if (n_refine_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_refine_steps < 0");
-    TRY(check_rule(refiner->cfg, rule));
-    if (workspace_bytes < dlm_cascade_workspace_bytes(&drafter->cfg, &refiner->cfg, batch, prompt_len, draft_len,
-                                                      block_len))
-        return fail(DLM_ERR_WORKSPACE, "workspace too small for the cascade");
-    using clk = std::chrono::steady_clock;
-    dlm_cascade_stats cs{};
-    const auto t0 = clk::now();
-    TRY(dlm_draft(drafter, batch, prompt_len, draft_len, d_prompt, d_draft, block_len, steps_per_block,
-                  draft_threshold, d_workspace, workspace_bytes, hip_stream, &cs.draft, nullptr));
-    const auto t1 = clk::now();              // dlm_draft returns with the draft written
-    TRY(dlm_refine_ex(refiner, batch, prompt_len, draft_len, d_prompt, d_draft, nullptr, n_refine_steps, rule,
-                      d_workspace, workspace_bytes, hip_stream, &cs.refine, &cs.refine_stop_reason));
-    const auto t2 = clk::now();              // and so does dlm_refine_ex
-    cs.draft_passes = cs.draft.steps_run;
-    cs.refine_passes = cs.refine.steps_run;
-    cs.draft_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
-    cs.refine_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
-    if (h_stats) *h_stats = cs;
-    return DLM_OK;
+    try {
+        if (!drafter || !refiner) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+        if (drafter->cfg.vocab != refiner->cfg.vocab || drafter->cfg.mask_id != refiner->cfg.mask_id)
+            return fail(DLM_ERR_INVALID_ARG, "drafter and refiner must share the vocabulary and the mask id");
+        if (n_refine_steps < 0) return fail(DLM_ERR_INVALID_ARG, "n_refine_steps < 0");
+        TRY(check_rule(refiner->cfg, rule));
+        if (workspace_bytes < dlm_cascade_workspace_bytes(&drafter->cfg, &refiner->cfg, batch, prompt_len, draft_len,
+                                                          block_len))
+            return fail(DLM_ERR_WORKSPACE, "workspace too small for the cascade");
+        using clk = std::chrono::steady_clock;
+        dlm_cascade_stats cs{};
+        const auto t0 = clk::now();
+        TRY(dlm_draft(drafter, batch, prompt_len, draft_len, d_prompt, d_draft, block_len, steps_per_block,
+                      draft_threshold, d_workspace, workspace_bytes, hip_stream, &cs.draft, nullptr));
+        const auto t1 = clk::now();              // dlm_draft returns with the draft written
+        TRY(dlm_refine_ex(refiner, batch, prompt_len, draft_len, d_prompt, d_draft, nullptr, n_refine_steps, rule,
+                          d_workspace, workspace_bytes, hip_stream, &cs.refine, &cs.refine_stop_reason));
+        const auto t2 = clk::now();              // and so does dlm_refine_ex
+        cs.draft_passes = cs.draft.steps_run;
+        cs.refine_passes = cs.refine.steps_run;
+        cs.draft_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+        cs.refine_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
+        if (h_stats) *h_stats = cs;
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_debug_forward(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                              const int32_t* d_tokens, void* d_workspace, size_t workspace_bytes,
                              void* hip_stream, float* d_hidden, float* d_max_logit, int32_t* d_top1,
                              float* d_conf, float* d_logits, int32_t* d_route_ids, float* d_router_logits) {
-    Workspace w;
-    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
-    if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
-    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
-    TRY(run_prologue(x, d_tokens));
-    const size_t route_words = (size_t)x.T * m->cfg.top_k;
-    for (int l = 0; l < m->cfg.n_layers; ++l) {
-        if (d_router_logits && m->cfg.n_experts > 0)
-            x.dbg_router_logits = d_router_logits + (size_t)l * x.T * m->cfg.n_experts;
-        TRY(run_layer(x, l));
-        if (d_route_ids && m->cfg.n_experts > 0)
-            HIP_TRY(hipMemcpyAsync(d_route_ids + l * route_words, x.at<int32_t>(w.ids), route_words * 4,
+    try {
+        Workspace w;
+        TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+        if (!d_tokens) return fail(DLM_ERR_INVALID_ARG, "tokens is NULL");
+        Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+        TRY(run_prologue(x, d_tokens));
+        const size_t route_words = (size_t)x.T * m->cfg.top_k;
+        for (int l = 0; l < m->cfg.n_layers; ++l) {
+            if (d_router_logits && m->cfg.n_experts > 0)
+                x.dbg_router_logits = d_router_logits + (size_t)l * x.T * m->cfg.n_experts;
+            TRY(run_layer(x, l));
+            if (d_route_ids && m->cfg.n_experts > 0)
+                HIP_TRY(hipMemcpyAsync(d_route_ids + l * route_words, x.at<int32_t>(w.ids), route_words * 4,
+                                       hipMemcpyDeviceToDevice, x.st));
+        }
+        if (d_hidden)
+            HIP_TRY(hipMemcpyAsync(d_hidden, x.at<float>(w.x), (size_t)x.T * m->cfg.d_model * 4,
                                    hipMemcpyDeviceToDevice, x.st));
+        if (d_max_logit || d_top1 || d_conf || d_logits) {
+            TRY(run_head(x, x.at<int32_t>(w.top1), x.at<float>(w.conf), x.at<float>(w.maxlogit), d_logits));
+            const size_t R = (size_t)x.R;
+            if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
+            if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
+            if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
+        }
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
     }
-    if (d_hidden)
-        HIP_TRY(hipMemcpyAsync(d_hidden, x.at<float>(w.x), (size_t)x.T * m->cfg.d_model * 4,
-                               hipMemcpyDeviceToDevice, x.st));
-    if (d_max_logit || d_top1 || d_conf || d_logits) {
-        TRY(run_head(x, x.at<int32_t>(w.top1), x.at<float>(w.conf), x.at<float>(w.maxlogit), d_logits));
-        const size_t R = (size_t)x.R;
-        if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
-        if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
-        if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
-    }
-    return DLM_OK;
 }
 
 dlm_status dlm_debug_layer(dlm_model* m, int32_t layer, int32_t batch, int32_t seq_len, const float* d_x_in,
                            float* d_x_out, void* d_workspace, size_t workspace_bytes, void* hip_stream,
                            int32_t* d_route_ids, float* d_router_logits) {
-    Workspace w;
-    TRY(check_common(m, batch, 0, seq_len, d_workspace, workspace_bytes, &w));
-    if (layer < 0 || layer >= m->cfg.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
-    if (!d_x_in || !d_x_out) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
-    Ctx x = ctx_for(m, batch, 0, seq_len, d_workspace, w, hip_stream);
-    if (m->cfg.n_experts > 0) x.dbg_router_logits = d_router_logits;
-    const size_t bytes = (size_t)x.T * m->cfg.d_model * 4;
-    HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x_in, bytes, hipMemcpyDeviceToDevice, x.st));
-    TRY(run_prologue(x, nullptr));
-    TRY(run_layer(x, layer));
-    HIP_TRY(hipMemcpyAsync(d_x_out, x.at<float>(w.x), bytes, hipMemcpyDeviceToDevice, x.st));
-    if (d_route_ids && m->cfg.n_experts > 0)
-        HIP_TRY(hipMemcpyAsync(d_route_ids, x.at<int32_t>(w.ids), (size_t)x.T * m->cfg.top_k * 4,
-                               hipMemcpyDeviceToDevice, x.st));
-    return DLM_OK;
+    try {
+        Workspace w;
+        TRY(check_common(m, batch, 0, seq_len, d_workspace, workspace_bytes, &w));
+        if (layer < 0 || layer >= m->cfg.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
+        if (!d_x_in || !d_x_out) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
+        Ctx x = ctx_for(m, batch, 0, seq_len, d_workspace, w, hip_stream);
+        if (m->cfg.n_experts > 0) x.dbg_router_logits = d_router_logits;
+        const size_t bytes = (size_t)x.T * m->cfg.d_model * 4;
+        HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x_in, bytes, hipMemcpyDeviceToDevice, x.st));
+        TRY(run_prologue(x, nullptr));
+        TRY(run_layer(x, layer));
+        HIP_TRY(hipMemcpyAsync(d_x_out, x.at<float>(w.x), bytes, hipMemcpyDeviceToDevice, x.st));
+        if (d_route_ids && m->cfg.n_experts > 0)
+            HIP_TRY(hipMemcpyAsync(d_route_ids, x.at<int32_t>(w.ids), (size_t)x.T * m->cfg.top_k * 4,
+                                   hipMemcpyDeviceToDevice, x.st));
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_debug_head(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len, const float* d_x,
                           void* d_workspace, size_t workspace_bytes, void* hip_stream, float* d_max_logit,
                           int32_t* d_top1, float* d_conf) {
-    Workspace w;
-    TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
-    if (!d_x) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
-    Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
-    HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x, (size_t)x.T * m->cfg.d_model * 4, hipMemcpyDeviceToDevice, x.st));
-    TRY(run_head(x, x.at<int32_t>(w.top1), x.at<float>(w.conf), x.at<float>(w.maxlogit), nullptr));
-    const size_t R = (size_t)x.R;
-    if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
-    if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
-    if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
-    return DLM_OK;
+    try {
+        Workspace w;
+        TRY(check_common(m, batch, prompt_len, draft_len, d_workspace, workspace_bytes, &w));
+        if (!d_x) return fail(DLM_ERR_INVALID_ARG, "x is NULL");
+        Ctx x = ctx_for(m, batch, prompt_len, draft_len, d_workspace, w, hip_stream);
+        HIP_TRY(hipMemcpyAsync(x.at<float>(w.x), d_x, (size_t)x.T * m->cfg.d_model * 4, hipMemcpyDeviceToDevice, x.st));
+        TRY(run_head(x, x.at<int32_t>(w.top1), x.at<float>(w.conf), x.at<float>(w.maxlogit), nullptr));
+        const size_t R = (size_t)x.R;
+        if (d_max_logit) HIP_TRY(hipMemcpyAsync(d_max_logit, x.at<float>(w.maxlogit), R * 4, hipMemcpyDeviceToDevice, x.st));
+        if (d_top1) HIP_TRY(hipMemcpyAsync(d_top1, x.at<int32_t>(w.top1), R * 4, hipMemcpyDeviceToDevice, x.st));
+        if (d_conf) HIP_TRY(hipMemcpyAsync(d_conf, x.at<float>(w.conf), R * 4, hipMemcpyDeviceToDevice, x.st));
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_debug_gemm(const void* d_a, const void* d_b, float* d_c, int32_t m, int32_t n, int32_t k,
                           int32_t tile_m, int32_t tile_n, void* hip_stream) {
-    if (!d_a || !d_b || !d_c) return fail(DLM_ERR_INVALID_ARG, "NULL argument");
-    if (m <= 0 || n <= 0 || k <= 0 || k % 64) return fail(DLM_ERR_INVALID_ARG, "bad GEMM shape");
-    GemmArgs a = gemm_args((const bf16_t*)d_a, k, (const bf16_t*)d_b, k, m, n, k);
-    a.out = d_c;
-    a.ldo = n;
-    a.variant = tile_m >> 16;
-    hipError_t e = launch_gemm(a, EPI_F32, false, tile_m & 0xffff, tile_n, 0, (hipStream_t)hip_stream);
-    if (e != hipSuccess) return fail(DLM_ERR_INVALID_ARG, std::string("gemm: ") + hipGetErrorString(e));
-    return DLM_OK;
+    try {
+        if (!d_a || !d_b || !d_c) return fail(DLM_ERR_INVALID_ARG, "NULL argument");
+        if (m <= 0 || n <= 0 || k <= 0 || k % 64) return fail(DLM_ERR_INVALID_ARG, "bad GEMM shape");
+        GemmArgs a = gemm_args((const bf16_t*)d_a, k, (const bf16_t*)d_b, k, m, n, k);
+        a.out = d_c;
+        a.ldo = n;
+        a.variant = tile_m >> 16;
+        hipError_t e = launch_gemm(a, EPI_F32, false, tile_m & 0xffff, tile_n, 0, (hipStream_t)hip_stream);
+        if (e != hipSuccess) return fail(DLM_ERR_INVALID_ARG, std::string("gemm: ") + hipGetErrorString(e));
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 dlm_status dlm_weight_info(dlm_model* m, int32_t layer_field, int32_t kind, int32_t expert, void** d_ptr,
                            int32_t* layout) {
-    if (!m || !d_ptr || !layout) return fail(DLM_ERR_INVALID_ARG, "NULL argument");
-    const dlm_config& c = m->cfg;
-    const size_t d = c.d_model;
-    if (layer_field == 0) {
-        if (kind == 0) { *d_ptr = m->base + m->plan.emb; *layout = 0; return DLM_OK; }
-        if (kind == 1) { *d_ptr = m->base + m->plan.lm; *layout = 0; return DLM_OK; }
-        return fail(DLM_ERR_INVALID_ARG, "unknown global tensor kind");
+    try {
+        if (!m || !d_ptr || !layout) return fail(DLM_ERR_INVALID_ARG, "NULL argument");
+        const dlm_config& c = m->cfg;
+        const size_t d = c.d_model;
+        if (layer_field == 0) {
+            if (kind == 0) { *d_ptr = m->base + m->plan.emb; *layout = 0; return DLM_OK; }
+            if (kind == 1) { *d_ptr = m->base + m->plan.lm; *layout = 0; return DLM_OK; }
+            return fail(DLM_ERR_INVALID_ARG, "unknown global tensor kind");
+        }
+        const int l = layer_field - 1;
+        if (l < 0 || l >= c.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
+        const LayerPtrs& L = m->plan.layers[l];
+        const size_t nq = (size_t)c.n_heads * c.head_dim, nk = (size_t)c.n_kv_heads * c.head_dim;
+        char* b = m->base;
+        *layout = 0;
+        switch (kind) {
+            case K_WQ: *d_ptr = b + L.wqkv; return DLM_OK;
+            case K_WK: *d_ptr = b + L.wqkv + nq * d * 2; return DLM_OK;
+            case K_WV: *d_ptr = b + L.wqkv + (nq + nk) * d * 2; return DLM_OK;
+            case K_WO: *d_ptr = b + L.wo; return DLM_OK;
+            default: break;
+        }
+        if (c.n_experts == 0) {
+            if (kind == K_FG || kind == K_FU) { *d_ptr = b + L.wgu; *layout = 1; return DLM_OK; }
+            if (kind == K_FD) { *d_ptr = b + L.wd; return DLM_OK; }
+            return fail(DLM_ERR_INVALID_ARG, "unknown dense-layer tensor kind");
+        }
+        const size_t F = c.expert_ffn_dim;
+        int e = expert;
+        if (kind == K_ROUTER) { *d_ptr = b + L.wr; return DLM_OK; }
+        if (kind >= K_SG && kind <= K_SD) {
+            if (expert < 0 || expert >= c.n_shared_experts) return fail(DLM_ERR_INVALID_ARG, "shared expert out of range");
+            e = c.n_experts + expert;
+            kind -= 3;
+        } else if (expert < 0 || expert >= c.n_experts) {
+            return fail(DLM_ERR_INVALID_ARG, "expert out of range");
+        }
+        if (kind == K_EG || kind == K_EU) { *d_ptr = b + L.wgu + (size_t)e * 2 * F * d * 2; *layout = 1; return DLM_OK; }
+        if (kind == K_ED) { *d_ptr = b + L.wd + (size_t)e * d * F * 2; return DLM_OK; }
+        return fail(DLM_ERR_INVALID_ARG, "unknown tensor kind");
+    } catch (...) {
+        return caught_exception();
     }
-    const int l = layer_field - 1;
-    if (l < 0 || l >= c.n_layers) return fail(DLM_ERR_INVALID_ARG, "layer out of range");
-    const LayerPtrs& L = m->plan.layers[l];
-    const size_t nq = (size_t)c.n_heads * c.head_dim, nk = (size_t)c.n_kv_heads * c.head_dim;
-    char* b = m->base;
-    *layout = 0;
-    switch (kind) {
-        case K_WQ: *d_ptr = b + L.wqkv; return DLM_OK;
-        case K_WK: *d_ptr = b + L.wqkv + nq * d * 2; return DLM_OK;
-        case K_WV: *d_ptr = b + L.wqkv + (nq + nk) * d * 2; return DLM_OK;
-        case K_WO: *d_ptr = b + L.wo; return DLM_OK;
-        default: break;
-    }
-    if (c.n_experts == 0) {
-        if (kind == K_FG || kind == K_FU) { *d_ptr = b + L.wgu; *layout = 1; return DLM_OK; }
-        if (kind == K_FD) { *d_ptr = b + L.wd; return DLM_OK; }
-        return fail(DLM_ERR_INVALID_ARG, "unknown dense-layer tensor kind");
-    }
-    const size_t F = c.expert_ffn_dim;
-    int e = expert;
-    if (kind == K_ROUTER) { *d_ptr = b + L.wr; return DLM_OK; }
-    if (kind >= K_SG && kind <= K_SD) {
-        if (expert < 0 || expert >= c.n_shared_experts) return fail(DLM_ERR_INVALID_ARG, "shared expert out of range");
-        e = c.n_experts + expert;
-        kind -= 3;
-    } else if (expert < 0 || expert >= c.n_experts) {
-        return fail(DLM_ERR_INVALID_ARG, "expert out of range");
-    }
-    if (kind == K_EG || kind == K_EU) { *d_ptr = b + L.wgu + (size_t)e * 2 * F * d * 2; *layout = 1; return DLM_OK; }
-    if (kind == K_ED) { *d_ptr = b + L.wd + (size_t)e * d * F * 2; return DLM_OK; }
-    return fail(DLM_ERR_INVALID_ARG, "unknown tensor kind");
 }
 
 dlm_status dlm_set_profiling(dlm_model* m, const char* name_filter) {
-    if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
-    m->prof_on = name_filter != nullptr;
-    m->prof_filter = name_filter ? name_filter : "";
-    m->prof_used = 0;
-    return DLM_OK;
+    try {
+        if (!m) return fail(DLM_ERR_INVALID_ARG, "model handle is NULL");
+        m->prof_on = name_filter != nullptr;
+        m->prof_filter = name_filter ? name_filter : "";
+        m->prof_used = 0;
+        return DLM_OK;
+    } catch (...) {
+        return caught_exception();
+    }
 }
 
 int32_t dlm_profile_read(dlm_model* m, const char** names, float* ms, int32_t max_entries) {
-    if (!m) return -1;
-    int32_t n = 0;
-    for (size_t i = 0; i < m->prof_used && n < max_entries; ++i) {
-        float t = 0.f;
-        if (hipEventSynchronize(m->prof[i].b) != hipSuccess) return -1;
-        if (hipEventElapsedTime(&t, m->prof[i].a, m->prof[i].b) != hipSuccess) return -1;
-        if (names) names[n] = m->prof[i].name;
-        if (ms) ms[n] = t;
-        ++n;
+    try {
+        if (!m) return -1;
+        int32_t n = 0;
+        for (size_t i = 0; i < m->prof_used && n < max_entries; ++i) {
+            float t = 0.f;
+            if (hipEventSynchronize(m->prof[i].b) != hipSuccess) return -1;
+            if (hipEventElapsedTime(&t, m->prof[i].a, m->prof[i].b) != hipSuccess) return -1;
+            if (names) names[n] = m->prof[i].name;
+            if (ms) ms[n] = t;
+            ++n;
+        }
+        return n;
+    } catch (...) {
+        caught_exception();
+        return -1;
     }
-    return n;
+}
+
+dlm_status dlm_debug_fail_host_alloc(int32_t n) {
+    if (n < 0) return fail(DLM_ERR_INVALID_ARG, "n must be >= 0");
+    g_fail_alloc_in.store(n, std::memory_order_relaxed);
+    return DLM_OK;
 }
 
 void dlm_free(dlm_model* m) {

@@ -102,6 +102,39 @@ def test_errors_are_reported_without_gpu_work():
         L.check(-1, "x")
 
 
+def test_host_allocation_failure_is_a_status():
+    """A failed host allocation inside the library (injected at its allocation
+    points) comes back as DLM_ERR_NO_MEMORY, leaves no half-built model behind,
+    and the next call works: no C++ exception crosses the C ABI."""
+    L = _lib()
+    lib = L.load()
+    cfg = _cfg(L)
+    wb = lib.dlm_weights_bytes(ctypes.byref(cfg))
+    assert wb > 0
+    try:
+        assert lib.dlm_debug_fail_host_alloc(1) == 0
+        assert lib.dlm_weights_bytes(ctypes.byref(cfg)) == 0
+        assert b"allocation" in lib.dlm_last_error()
+        assert lib.dlm_weights_bytes(ctypes.byref(cfg)) == wb            # the hook fired once
+        # The weight plan is built before any GPU work; with the hook off the
+        # same call stops at the size check (weights_bytes 0), so no GPU work
+        # is launched either way.
+        h = ctypes.c_void_p(1)
+        assert lib.dlm_debug_fail_host_alloc(1) == 0
+        st = lib.dlm_load_synthetic_weights(ctypes.byref(cfg), 0, ctypes.c_void_p(256), 0, None, ctypes.byref(h))
+        assert st == -6 and h.value is None, (st, h.value)
+        assert L.STATUS_NAMES[st] == "DLM_ERR_NO_MEMORY"
+        st = lib.dlm_load_synthetic_weights(ctypes.byref(cfg), 0, ctypes.c_void_p(256), 0, None, ctypes.byref(h))
+        assert st == -5
+        # a later allocation point: the second pass through one fails
+        assert lib.dlm_debug_fail_host_alloc(2) == 0
+        assert lib.dlm_weights_bytes(ctypes.byref(cfg)) == wb
+        assert lib.dlm_weights_bytes(ctypes.byref(cfg)) == 0
+        assert lib.dlm_debug_fail_host_alloc(-1) == -1
+    finally:
+        lib.dlm_debug_fail_host_alloc(0)
+
+
 def test_bench_refuses_more_than_one_gpu():
     """bench.py runs on one GPU: --gpus 2 exits with status 2 and says why,
     before any GPU work."""

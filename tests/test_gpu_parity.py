@@ -173,6 +173,34 @@ def test_refine_tiny_free_running(tiny_sharp, seed, tau):
     assert gst["n_masked_left"] == st["n_masked_left"] and gst["n_invalid"] == 0
 
 
+@pytest.mark.parametrize("n1", [1, 2])
+def test_refine_resume_equals_one_longer_refine(tiny_sharp, n1):
+    """The refinement state is the token array: refine(n1) followed by
+    refine(n2) on its result (still-masked slots hold mask_id) ends on the
+    same draft as one refine(n1 + n2), with the same numbers of unmasked and
+    edited slots (Sec. 4.2: each pass reads only the current sequence; the
+    pass budget is an upper bound with an early stop).  The second part may
+    run one more pass, the one that finds nothing left to change."""
+    torch = _torch()
+    w, s, R, W = tiny_sharp
+    seed, tau = FREE_RUNNING[0]
+    prompt, draft, mask = make_inputs(w, seed=seed)
+    n = w.n_steps
+    d_prompt, d_mask = _cuda_i32(prompt), torch.tensor(mask, device="cuda")
+    whole = _cuda_i32(draft)
+    _, g_all = R.refine(d_prompt, whole, d_mask, n, tau)
+    part = _cuda_i32(draft)
+    _, g1 = R.refine(d_prompt, part, d_mask, n1, tau)
+    _, g2 = R.refine(d_prompt, part, None, n - n1, tau)
+    log(f"[resume n1 {n1} of {n}] whole {g_all}; parts {g1} + {g2}")
+    assert g_all["n_unmasked"] + g_all["n_edited"] > 0
+    assert np.array_equal(_np(part), _np(whole))
+    assert g1["n_unmasked"] + g2["n_unmasked"] == g_all["n_unmasked"]
+    assert g1["n_edited"] + g2["n_edited"] == g_all["n_edited"]
+    assert g_all["steps_run"] <= g1["steps_run"] + g2["steps_run"] <= g_all["steps_run"] + 1
+    assert g2["n_masked_left"] == g_all["n_masked_left"]
+
+
 def test_refine_tiny_sharp_trajectory(tiny_sharp):
     """Edits happen (sharp LM head).  Along the GPU's own trajectory every pass is
     compared with the oracle's pass on the same input: decisions and top-1 agree
