@@ -17,6 +17,8 @@ prompt 0-80, draft 1-100 tokens, some [MASK] slots).  Per case:
 
 from __future__ import annotations
 
+import os
+
 import numpy as np
 import pytest
 
@@ -26,36 +28,53 @@ from workloads.inputs import draw_tokens
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 16
+# The committed sweep runs 16 cases; DLM_SWEEP_CASES widens it for a longer
+# one-off run (the cases are the same seeded draws, extended).
+N_CASES = int(os.environ.get("DLM_SWEEP_CASES", "48"))
+# Larger shapes (more K tiles, more experts and tokens per case), fewer of them.
+N_BIG = int(os.environ.get("DLM_SWEEP_BIG_CASES", "6"))
 
 
-def _case(i):
-    rng = np.random.default_rng(1000 + i)
+def _case(i, big=False):
+    rng = np.random.default_rng((5000 if big else 1000) + i)
     hd = int(rng.choice([64, 128]))
     while True:
         kv = int(rng.integers(1, 5))
         h = kv * int(rng.integers(1, 5))
         if (h * hd) % 128 == 0 and (kv * hd) % 128 == 0:
             break
-    over = dict(n_layers=int(rng.integers(1, 3)), d_model=int(rng.choice([128, 256, 384, 512])), n_heads=h,
-                n_kv_heads=kv, head_dim=hd, vocab=int(rng.integers(64, 3000)))
+    dims = [768, 1024] if big else [128, 256, 384, 512]
+    over = dict(n_layers=int(rng.integers(1, 4 if big else 3)), d_model=int(rng.choice(dims)), n_heads=h,
+                n_kv_heads=kv, head_dim=hd, vocab=int(rng.integers(64, 9000 if big else 3000)))
     if rng.random() < 0.7:
-        e = int(rng.integers(2, 33))
+        e = int(rng.integers(2, 65 if big else 33))
         over.update(ffn_dim=0, n_experts=e, top_k=int(rng.integers(1, min(8, e) + 1)),
-                    expert_ffn_dim=64 * int(rng.integers(1, 5)), n_shared_experts=int(rng.integers(0, 2)))
+                    expert_ffn_dim=64 * int(rng.integers(1, 9 if big else 5)), n_shared_experts=int(rng.integers(0, 2)))
     else:
-        over.update(ffn_dim=64 * int(rng.integers(1, 9)), n_experts=0, top_k=0, expert_ffn_dim=0, n_shared_experts=0)
-    B, P, D = int(rng.integers(1, 4)), int(rng.integers(0, 81)), int(rng.integers(1, 101))
-    return MODELS["tiny"].replace(**over), B, P, D, 2000 + i
+        over.update(ffn_dim=64 * int(rng.integers(1, 17 if big else 9)), n_experts=0, top_k=0, expert_ffn_dim=0,
+                    n_shared_experts=0)
+    if big:
+        B, P, D = int(rng.integers(1, 5)), int(rng.integers(0, 201)), int(rng.integers(1, 201))
+    else:
+        B, P, D = int(rng.integers(1, 4)), int(rng.integers(0, 81)), int(rng.integers(1, 101))
+    return MODELS["tiny"].replace(**over), B, P, D, (6000 if big else 2000) + i
 
 
 @pytest.mark.parametrize("i", range(N_CASES))
 def test_random_shape(i):
+    _check(*_case(i), f"sweep {i}")
+
+
+@pytest.mark.parametrize("i", range(N_BIG))
+def test_random_larger_shape(i):
+    _check(*_case(i, big=True), f"sweep big {i}")
+
+
+def _check(shape, B, P, D, seed, tag):
     need_gpu()
     import torch
     import oracle
     from paper_2608_02625_amd import Refiner
-    shape, B, P, D, seed = _case(i)
     R = Refiner(shape.as_dict(), seed)
     W = oracle.OracleWeights(shape, seed)
     rng = np.random.default_rng(seed)
@@ -93,7 +112,7 @@ def test_random_shape(i):
     R.refine_step(g.clone(), P, 1.5, top1=t1, conf=cf)
     torch.cuda.synchronize()
     same = bool(torch.equal(t1, out["top1"]) and torch.equal(cf, out["conf"]))
-    log(f"[sweep {i}] L{shape.n_layers} d{d} H{shape.n_heads}/{shape.n_kv_heads}x{shape.head_dim} "
+    log(f"[{tag}] L{shape.n_layers} d{d} H{shape.n_heads}/{shape.n_kv_heads}x{shape.head_dim} "
         f"E{shape.n_experts}k{shape.top_k}F{shape.expert_ffn_dim or shape.ffn_dim}s{shape.n_shared_experts} "
         f"V{shape.vocab} B{B} P{P} D{D}: hidden {eh:.2e} on {int(alike.sum())}/{T} (routing differs for {n_flip}); "
         f"top1 checked {int(keep_d.sum())} mismatches {mism}; step == forward {same}")
