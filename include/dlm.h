@@ -143,6 +143,10 @@ dlm_status dlm_load_synthetic_weights(const dlm_config* cfg, uint64_t seed, void
  *   fields 0).
  * threshold must not be NaN (any other float is accepted; > 1 edits nothing,
  * <= 0 takes every top-1 that is not mask_id).
+ * The call only enqueues kernels and device-to-device copies on hip_stream;
+ * it allocates nothing, records no memset and never waits on the host, so it
+ * may be captured in a HIP graph (stream capture) and replayed (as may
+ * dlm_refine_step_static and dlm_refine_step_ex).
  */
 dlm_status dlm_refine_step(dlm_model* m, int32_t batch, int32_t prompt_len, int32_t draft_len,
                            int32_t* d_tokens, float threshold, void* d_workspace,
