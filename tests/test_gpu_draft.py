@@ -385,3 +385,43 @@ def test_draft_flash_slice_properties():
     assert np.array_equal(_np(short), _np(a)[:, :64])
     assert sa["n_masked_left"] == 0
     del R
+
+
+def _dense_case(i):
+    rng = np.random.default_rng(3000 + i)
+    hd = int(rng.choice([64, 128]))
+    while True:
+        kv = int(rng.integers(1, 5))
+        h = kv * int(rng.integers(1, 4))
+        if (h * hd) % 128 == 0 and (kv * hd) % 128 == 0:
+            break
+    over = dict(n_layers=int(rng.integers(1, 3)), d_model=int(rng.choice([128, 256, 384])), n_heads=h, n_kv_heads=kv,
+                head_dim=hd, vocab=int(rng.integers(64, 2000)), ffn_dim=64 * int(rng.integers(1, 9)), n_experts=0,
+                top_k=0, expert_ffn_dim=0, n_shared_experts=0, lm_head_scale=10.0)
+    B, P = int(rng.integers(1, 4)), int(rng.integers(0, 40))
+    b = int(rng.choice([4, 8, 16, 32]))
+    D = int(rng.integers(1, 3 * b + 1))
+    steps = int(rng.integers(1, 5))
+    tau = float(rng.choice([0.25, 0.5, 0.9, 2.0]))
+    return over, B, P, D, b, steps, tau, 4000 + i
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_draft_random_dense_shapes(i):
+    """Seeded random dense shapes (d_model 128-384, head_dim 64/128, 1-12 query
+    heads over 1-4 KV heads, 1-2 blocks, vocabularies of 64-2000, sharpened
+    head), ragged batches and block settings (blocks of 4-32, 1-4 steps,
+    thresholds 0.25-2.0): every step against the oracle's step on the same
+    tokens, and the loop equal to the step-by-step trajectory."""
+    need_gpu()
+    import oracle
+    from paper_2608_02625_amd import Refiner
+    over, B, P, D, b, steps, tau, seed = _dense_case(i)
+    s = WORKLOADS["tiny"].model.replace(**over)
+    R = Refiner(s.as_dict(), seed)
+    W = oracle.OracleWeights(s, seed)
+    prompt = _prompts(s.vocab, B, P, seed)
+    tag = (f"draft sweep {i}: L{s.n_layers} d{s.d_model} H{s.n_heads}/{s.n_kv_heads}x{s.head_dim} F{s.ffn_dim} "
+           f"V{s.vocab} B{B} P{P} D{D} b{b} s{steps} t{tau}")
+    checked, bs = _trajectory(R, W, s, prompt, D, b, steps, tau, MARGIN * s.lm_head_scale, tag)
+    assert len(bs) == -(-D // b) and checked > 0
